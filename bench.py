@@ -1,0 +1,183 @@
+#!/usr/bin/env python3
+"""Benchmark of the fused vocabulary-projection cross-entropy (forward + backward) on one MI355X.
+
+A step is one pass of the whole path over one batch: the fused forward (logits
+tiles folded into the online log-sum-exp, target gather, split combine) and the
+backward (logits recompute, softmax residual, dH and dW contractions), through
+the C ABI on torch's current stream, inputs resident in HBM.
+
+Prints ONE JSON line: tokens/s of the whole job (value), ms per step, achieved
+TFLOP/s counted as 8*T*V*d per step (2TVd forward, 6TVd backward with recompute)
+against the dense bf16 MFMA peak, the working set, a roofline entry for the
+fused forward kernel (timed with HIP events on the launch stream) and the CPU
+oracle timed on a bounded row sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2516.6  # MI355X dense bf16 MFMA: 256 CU x 2.4 GHz x 4096 flop/clk
+PEAK_F32_TFLOPS = 157.3    # MI355X fp32 (MFMA/vector)
+PEAK_HBM_GBS = 8000.0
+DEFAULT_WORKLOAD = "longctx_bf16_T32768_d2880_V201088_P8_ring"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
+    ap.add_argument("--cpu-sample-rows", type=int, default=256,
+                    help="token rows of the workload the CPU oracle is timed on")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--strip-elems", type=int, default=0)
+    return ap.parse_args()
+
+
+def cpu_baseline(inp, rows: int):
+    """The oracle as it stands, on the first `rows` tokens (full V and d): its cost is linear in T."""
+    import numpy as np
+
+    import oracle
+    import workloads as wl
+
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        cores = os.cpu_count() or 1
+    rows = min(rows, inp.T)
+    H = wl.to_f64(inp.H[:rows], inp.dtype)
+    Ws = [wl.to_f64(w, inp.dtype) for w in inp.W_shards]
+    g = wl.random_grad_loss(rows, 0, "sum")
+    t0 = time.perf_counter()
+    oracle.forward_backward(H, Ws, inp.targets[:rows], g, inp.ignore_index)
+    dt = time.perf_counter() - t0
+    return {"value": rows / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
+            "sample": f"first {rows} of {inp.T} tokens at full V={inp.V}, d={inp.d} "
+                      f"(float64 forward+backward, {dt:.2f} s)",
+            "seconds": dt}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on exactly one GPU (one device's share of "
+                                   "the ring); --gpus must be 1", "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+
+    import paper_2609_14306_amd as vp
+    import workloads as wl
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    w = wl.WORKLOADS[args.workload]
+    t_gen = time.perf_counter()
+    inp = wl.make_inputs(w)
+    t_gen = time.perf_counter() - t_gen
+
+    def to_dev(x):
+        if inp.dtype == "bf16":
+            return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).to(dev).view(torch.bfloat16)
+        return torch.from_numpy(np.ascontiguousarray(x)).to(dev)
+
+    H = to_dev(inp.H)
+    Ws = [to_dev(x) for x in inp.W_shards]
+    tg = torch.from_numpy(inp.targets).to(dev)
+    T, d, V = inp.T, inp.d, inp.V
+    n_valid = int((inp.targets != inp.ignore_index).sum())
+    g = torch.full((T,), 1.0 / max(n_valid, 1), dtype=torch.float32, device=dev)
+    prob = vp.problem_for(H, Ws, inp.ignore_index, inp.order, 0, args.strip_elems)
+    fwd_b, bwd_b = vp.vp_ce_workspace_size(prob)
+    ws = torch.empty(max(fwd_b, bwd_b), dtype=torch.uint8, device=dev)
+    loss = torch.empty(T, dtype=torch.float32, device=dev)
+    lse = torch.empty(T, dtype=torch.float32, device=dev)
+    dH = torch.empty(T, d, dtype=torch.float32, device=dev)
+    dWs = [torch.empty(x.shape[0], d, dtype=torch.float32, device=dev) for x in Ws]
+    stream = torch.cuda.current_stream()
+
+    def step(ev=None):
+        if ev is not None:
+            ev[0].record(stream)
+        vp.vp_ce_forward(prob, H, Ws, tg, loss, lse, ws)
+        if ev is not None:
+            ev[1].record(stream)
+        vp.vp_ce_backward(prob, H, Ws, tg, lse, g, dH, dWs, ws)
+        if ev is not None:
+            ev[2].record(stream)
+
+    torch.cuda.synchronize()
+    base_alloc = torch.cuda.memory_allocated()
+    torch.cuda.reset_peak_memory_stats()
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    bad = vp.vp_ce_check(ws)
+    extra_alloc = torch.cuda.max_memory_allocated() - base_alloc
+
+    evs = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for k in range(args.steps):
+        step(evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
+    bwd_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    gpu_ms = evs[0][0].elapsed_time(evs[-1][2]) / args.steps
+    ms_per_step = max(wall * 1e3 / args.steps, gpu_ms)
+    flops = 8.0 * T * V * d
+    tflops = flops / (ms_per_step * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if inp.dtype == "bf16" else PEAK_F32_TFLOPS
+    fwd_avg = float(np.mean(fwd_ms))
+    fwd_tflops = 2.0 * T * V * d / (fwd_avg * 1e-3) / 1e12
+
+    out = {
+        "metric": "vocab-proj CE fwd+bwd tokens/s; % bf16 MFMA peak; peak working set MiB",
+        "value": T / (ms_per_step * 1e-3),
+        "unit": "tokens/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": inp.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "T": T, "d": d, "V": V, "P": len(Ws), "order": inp.order,
+                   "target_law": w.target_law, "ignore_frac": w.ignore_frac,
+                   "parallelism": "single GPU (one rank's share of the ring)"},
+        "tflops": tflops,
+        "pct_peak": 100.0 * tflops / peak,
+        "fwd_ms": fwd_avg,
+        "bwd_ms": float(np.mean(bwd_ms)),
+        "working_set_mib": {"workspace_fwd": fwd_b / 2**20, "workspace_bwd": bwd_b / 2**20,
+                            "allocated_during_steps": extra_alloc / 2**20,
+                            "peak_over_resident": (max(fwd_b, bwd_b) + extra_alloc) / 2**20},
+        "roofline": {"kernel": "fwd_kernel (fused logits tiles + online LSE fold)",
+                     "bound": "mfma", "achieved": fwd_tflops, "peak": peak, "unit": "TFLOP/s",
+                     "frac": fwd_tflops / peak, "traffic": None},
+        "bad_targets": bad,
+        "input_gen_s": t_gen,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline(inp, args.cpu_sample_rows)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,332 @@
+// Host side of the C ABI declared in include/vpce.h: argument validation,
+// workspace planning and launch sequencing.  Every argument, shape, alignment
+// and workspace error is detected here before any HIP call is made, so these
+// paths run (and are tested) on a machine without a GPU.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+#include <string.h>
+
+#include <algorithm>
+#include <cmath>
+
+#include "vpce_internal.h"
+
+namespace {
+
+constexpr size_t kHeaderBytes = 256;       // error counter + reserved
+constexpr int64_t kDefaultStrip = 64ll << 20;  // residual-strip budget in elements
+constexpr int kTargetGroups = 512;         // forward workgroups to aim for (2 per CU on 256 CUs)
+constexpr int kMaxSplits = 32;
+
+inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+inline int64_t round_up(int64_t x, int64_t m) { return (x + m - 1) / m * m; }
+inline int64_t round_down(int64_t x, int64_t m) { return x / m * m; }
+inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
+
+size_t elem_bytes(int dtype) { return dtype == VP_BF16 ? 2 : 4; }
+
+vp_status validate(const vp_problem* p, int64_t* V_out) {
+  if (!p) return VP_ERR_NULL;
+  if (p->dtype != VP_F32 && p->dtype != VP_BF16) return VP_ERR_DTYPE;
+  if (p->T < 0 || p->d < 8 || p->d % 8 != 0 || p->d > (1ll << 30)) return VP_ERR_SHAPE;
+  if (p->T > (1ll << 30)) return VP_ERR_SHAPE;
+  if (p->P < 1 || p->P > VP_MAX_SHARDS) return VP_ERR_SHAPE;
+  if (!p->shard_rows) return VP_ERR_NULL;
+  if (p->strip_elems < 0) return VP_ERR_SHAPE;
+  int64_t V = 0;
+  for (int i = 0; i < p->P; ++i) {
+    if (p->shard_rows[i] < 0 || p->shard_rows[i] > (1ll << 30)) return VP_ERR_SHAPE;
+    V += p->shard_rows[i];
+  }
+  if (V < 1 || V > (1ll << 31) - 1) return VP_ERR_SHAPE;
+  if (p->order) {
+    bool seen[VP_MAX_SHARDS] = {false};
+    for (int i = 0; i < p->P; ++i) {
+      const int q = p->order[i];
+      if (q < 0 || q >= p->P || seen[q]) return VP_ERR_ORDER;
+      seen[q] = true;
+    }
+  }
+  if (V_out) *V_out = V;
+  return VP_OK;
+}
+
+inline bool misaligned(const void* ptr) { return ((uintptr_t)ptr & 15u) != 0; }
+
+int splits_for(const vp_problem* p) {
+  const vpce::TileShape ts = vpce::tile_shape(p->dtype);
+  const int64_t tok_blocks = std::max<int64_t>(1, ceil_div(p->T, ts.fwd_bn));
+  return (int)std::min<int64_t>(kMaxSplits, std::max<int64_t>(1, ceil_div(kTargetGroups, tok_blocks)));
+}
+
+size_t fwd_ws_bytes(const vp_problem* p) {
+  const size_t T = (size_t)p->T;
+  const size_t S = (size_t)splits_for(p);
+  return kHeaderBytes + 2 * align256(S * T * 4) + align256(T * 4);
+}
+
+// Backward strip plan: Tc tokens by Vc vocabulary rows, Tc*Vc <= budget,
+// as square as the token count allows (this minimises the float32
+// read-modify-write traffic of dH across vocabulary chunks plus that of dW
+// across token chunks, which is proportional to 1/Vc + 1/Tc).
+struct StripPlan {
+  int64_t Tc, Vc, ldg;
+};
+
+StripPlan strip_plan(const vp_problem* p) {
+  const vpce::TileShape ts = vpce::tile_shape(p->dtype);
+  const int64_t budget = p->strip_elems > 0 ? p->strip_elems : kDefaultStrip;
+  const int64_t Tpad = round_up(std::max<int64_t>(p->T, 1), ts.grad_bn);
+  const int64_t side = round_down((int64_t)std::sqrt((double)budget), ts.grad_bn);
+  StripPlan s;
+  s.Tc = std::max<int64_t>(ts.grad_bn, std::min<int64_t>(Tpad, side));
+  s.ldg = s.Tc;
+  s.Vc = std::max<int64_t>(ts.grad_bm, std::min<int64_t>(round_down(budget / s.Tc, ts.grad_bm),
+                                                        1ll << 20));
+  return s;
+}
+
+size_t bwd_ws_bytes(const vp_problem* p) {
+  const StripPlan s = strip_plan(p);
+  return kHeaderBytes + align256((size_t)s.Vc * (size_t)s.ldg * elem_bytes(p->dtype));
+}
+
+void build_table(const vp_problem* p, const void* const* W_shards, int bm, vpce::ShardTable* st,
+                 int32_t* n_tiles) {
+  int64_t off[VP_MAX_SHARDS];
+  int64_t acc = 0;
+  for (int q = 0; q < p->P; ++q) {
+    off[q] = acc;
+    acc += p->shard_rows[q];
+  }
+  st->P = p->P;
+  int32_t tiles = 0;
+  for (int i = 0; i < p->P; ++i) {
+    const int q = p->order ? p->order[i] : i;
+    st->w[i] = W_shards[q];
+    st->off[i] = off[q];
+    st->rows[i] = (int32_t)p->shard_rows[q];
+    st->tile0[i] = tiles;
+    tiles += (int32_t)ceil_div(p->shard_rows[q], bm);
+  }
+  for (int i = p->P; i <= VP_MAX_SHARDS; ++i) st->tile0[i] = tiles;
+  for (int i = p->P; i < VP_MAX_SHARDS; ++i) {
+    st->w[i] = nullptr;
+    st->off[i] = acc;
+    st->rows[i] = 0;
+  }
+  *n_tiles = tiles;
+}
+
+vp_status check_shards(const vp_problem* p, const void* const* W_shards) {
+  if (!W_shards) return VP_ERR_NULL;
+  for (int q = 0; q < p->P; ++q) {
+    if (p->shard_rows[q] > 0 && !W_shards[q]) return VP_ERR_NULL;
+    if (p->shard_rows[q] > 0 && misaligned(W_shards[q])) return VP_ERR_ALIGN;
+  }
+  return VP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int vp_abi_version(void) { return VPCE_ABI_VERSION; }
+
+const char* vp_status_str(vp_status s) {
+  switch (s) {
+    case VP_OK: return "ok";
+    case VP_ERR_NULL: return "a required pointer is NULL";
+    case VP_ERR_SHAPE: return "invalid shape (T, d, P or shard rows)";
+    case VP_ERR_DTYPE: return "unsupported dtype";
+    case VP_ERR_ORDER: return "order is not a permutation of the shards";
+    case VP_ERR_ALIGN: return "a device pointer is not 16-byte aligned";
+    case VP_ERR_WORKSPACE: return "workspace missing or too small";
+    case VP_ERR_TARGET: return "a target is outside [0, V) and not ignore_index";
+    case VP_ERR_HIP: return "HIP runtime or kernel launch failure";
+    case VP_ERR_UNSUPPORTED: return "unsupported request";
+  }
+  return "unknown status";
+}
+
+vp_status vp_ce_workspace_size(const vp_problem* prob, size_t* fwd_bytes, size_t* bwd_bytes) {
+  const vp_status st = validate(prob, nullptr);
+  if (st != VP_OK) return st;
+  if (fwd_bytes) *fwd_bytes = fwd_ws_bytes(prob);
+  if (bwd_bytes) *bwd_bytes = bwd_ws_bytes(prob);
+  return VP_OK;
+}
+
+vp_status vp_ce_forward(const vp_problem* prob, const void* H, const void* const* W_shards,
+                        const int64_t* targets, float* loss, float* lse, void* ws,
+                        size_t ws_bytes, void* stream) {
+  int64_t V = 0;
+  vp_status st = validate(prob, &V);
+  if (st != VP_OK) return st;
+  if ((st = check_shards(prob, W_shards)) != VP_OK) return st;
+  if (!ws) return VP_ERR_WORKSPACE;
+  if (ws_bytes < fwd_ws_bytes(prob)) return VP_ERR_WORKSPACE;
+  if (misaligned(ws)) return VP_ERR_ALIGN;
+  const int64_t T = prob->T;
+  if (T > 0) {
+    if (!H || !targets || !loss || !lse) return VP_ERR_NULL;
+    if (misaligned(H)) return VP_ERR_ALIGN;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  unsigned long long* counter = (unsigned long long*)ws;
+  if (!vpce::run_ws_init(counter, s)) return VP_ERR_HIP;
+  if (T == 0) return VP_OK;
+
+  const vpce::TileShape ts = vpce::tile_shape(prob->dtype);
+  const int S = splits_for(prob);
+  char* base = (char*)ws + kHeaderBytes;
+  vpce::FwdArgs a;
+  memset(&a, 0, sizeof(a));
+  build_table(prob, W_shards, ts.fwd_bm, &a.st, &a.n_tiles);
+  a.H = H;
+  a.targets = targets;
+  a.T = T;
+  a.d = (int32_t)prob->d;
+  a.n_tok_blocks = (int32_t)ceil_div(T, ts.fwd_bn);
+  a.n_splits = S;
+  a.m_part = (float*)base;
+  a.s_part = (float*)(base + align256((size_t)S * T * 4));
+  a.y_tgt = (float*)(base + 2 * align256((size_t)S * T * 4));
+  if (!vpce::run_fwd(prob->dtype, a, s)) return VP_ERR_HIP;
+
+  vpce::CombArgs c;
+  c.m_part = a.m_part;
+  c.s_part = a.s_part;
+  c.y_tgt = a.y_tgt;
+  c.targets = targets;
+  c.T = T;
+  c.V = V;
+  c.ignore_index = prob->ignore_index;
+  c.n_splits = S;
+  c.loss = loss;
+  c.lse = lse;
+  c.bad_counter = counter;
+  if (!vpce::run_comb(c, s)) return VP_ERR_HIP;
+  return VP_OK;
+}
+
+vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* const* W_shards,
+                         const int64_t* targets, const float* lse, const float* grad_loss,
+                         float* dH, float* const* dW_shards, void* ws, size_t ws_bytes,
+                         void* stream) {
+  int64_t V = 0;
+  vp_status st = validate(prob, &V);
+  if (st != VP_OK) return st;
+  if ((st = check_shards(prob, W_shards)) != VP_OK) return st;
+  if (!dW_shards) return VP_ERR_NULL;
+  for (int q = 0; q < prob->P; ++q) {
+    if (prob->shard_rows[q] > 0 && !dW_shards[q]) return VP_ERR_NULL;
+    if (prob->shard_rows[q] > 0 && misaligned(dW_shards[q])) return VP_ERR_ALIGN;
+  }
+  if (!ws) return VP_ERR_WORKSPACE;
+  if (ws_bytes < bwd_ws_bytes(prob)) return VP_ERR_WORKSPACE;
+  if (misaligned(ws)) return VP_ERR_ALIGN;
+  const int64_t T = prob->T;
+  if (T > 0) {
+    if (!H || !targets || !lse || !grad_loss || !dH) return VP_ERR_NULL;
+    if (misaligned(H) || misaligned(dH)) return VP_ERR_ALIGN;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  unsigned long long* counter = (unsigned long long*)ws;
+  if (!vpce::run_ws_init(counter, s)) return VP_ERR_HIP;
+  const bool accumulate = (prob->flags & VP_ACCUMULATE_DW) != 0;
+  const int64_t d = prob->d;
+
+  if (T == 0) {  // G is empty: dW = 0 (or unchanged when accumulating); dH has no rows
+    if (!accumulate)
+      for (int q = 0; q < prob->P; ++q)
+        if (!vpce::run_fill_zero(dW_shards[q], prob->shard_rows[q] * d, s)) return VP_ERR_HIP;
+    return VP_OK;
+  }
+  if (!vpce::run_count_bad(targets, T, V, prob->ignore_index, counter, s)) return VP_ERR_HIP;
+
+  const vpce::TileShape ts = vpce::tile_shape(prob->dtype);
+  const StripPlan plan = strip_plan(prob);
+  void* strip = (char*)ws + kHeaderBytes;
+  const size_t eb = elem_bytes(prob->dtype);
+
+  int64_t off[VP_MAX_SHARDS];
+  int64_t acc = 0;
+  for (int q = 0; q < prob->P; ++q) {
+    off[q] = acc;
+    acc += prob->shard_rows[q];
+  }
+  bool first_vchunk = true;
+  for (int i = 0; i < prob->P; ++i) {
+    const int q = prob->order ? prob->order[i] : i;
+    const int64_t Vq = prob->shard_rows[q];
+    for (int64_t v0 = 0; v0 < Vq; v0 += plan.Vc) {
+      const int64_t M = std::min<int64_t>(plan.Vc, Vq - v0);
+      const char* Wc = (const char*)W_shards[q] + (size_t)v0 * d * eb;
+      float* dWc = dW_shards[q] + v0 * d;
+      for (int64_t t0 = 0; t0 < T; t0 += plan.Tc) {
+        const int64_t N = std::min<int64_t>(plan.Tc, T - t0);
+        vpce::GradArgs g;
+        g.W = Wc;
+        g.H = H;
+        g.targets = targets;
+        g.lse = lse;
+        g.grad = grad_loss;
+        g.strip = strip;
+        g.ldg = plan.ldg;
+        g.t0 = t0;
+        g.gid0 = off[q] + v0;
+        g.V = V;
+        g.ignore_index = prob->ignore_index;
+        g.M = (int32_t)M;
+        g.N = (int32_t)N;
+        g.d = (int32_t)d;
+        g.n_vt = (int32_t)ceil_div(M, ts.grad_bm);
+        if (!vpce::run_grad(prob->dtype, g, s)) return VP_ERR_HIP;
+
+        vpce::GemmArgs h;  // dH[t0 : t0+N] (+)= G^T W_chunk
+        h.A = strip;
+        h.lda = plan.ldg;
+        h.B = Wc;
+        h.ldb = d;
+        h.C = dH + t0 * d;
+        h.ldc = d;
+        h.M = (int32_t)N;
+        h.N = (int32_t)d;
+        h.K = (int32_t)M;
+        h.beta = first_vchunk ? 0 : 1;
+        h.n_nt = 0;
+        if (!vpce::run_dH(prob->dtype, h, s)) return VP_ERR_HIP;
+
+        vpce::GemmArgs w;  // dW_chunk (+)= G H[t0 : t0+N]
+        w.A = strip;
+        w.lda = plan.ldg;
+        w.B = (const char*)H + (size_t)t0 * d * eb;
+        w.ldb = d;
+        w.C = dWc;
+        w.ldc = d;
+        w.M = (int32_t)M;
+        w.N = (int32_t)d;
+        w.K = (int32_t)N;
+        w.beta = (t0 > 0 || accumulate) ? 1 : 0;
+        w.n_nt = 0;
+        if (!vpce::run_dW(prob->dtype, w, s)) return VP_ERR_HIP;
+      }
+      first_vchunk = false;
+    }
+  }
+  return VP_OK;
+}
+
+vp_status vp_ce_check(const void* ws, void* stream, int64_t* bad_targets) {
+  if (!ws) return VP_ERR_NULL;
+  unsigned long long count = 0;
+  hipStream_t s = (hipStream_t)stream;
+  if (hipMemcpyAsync(&count, ws, sizeof(count), hipMemcpyDeviceToHost, s) != hipSuccess)
+    return VP_ERR_HIP;
+  if (hipStreamSynchronize(s) != hipSuccess) return VP_ERR_HIP;
+  if (bad_targets) *bad_targets = (int64_t)count;
+  return count ? VP_ERR_TARGET : VP_OK;
+}
+
+}  // extern "C"

@@ -1,0 +1,89 @@
+// Internal interface between the host API (vpce_api.cpp) and the kernels.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include <algorithm>
+
+#include "vpce.h"
+
+namespace vpce {
+
+// Vocabulary shards in visiting order: position i is shard order[i].
+struct ShardTable {
+  const void* w[VP_MAX_SHARDS];   // device [rows[i], d]
+  int64_t off[VP_MAX_SHARDS];     // global id of the shard's first row
+  int32_t rows[VP_MAX_SHARDS];    // V_p
+  int32_t tile0[VP_MAX_SHARDS + 1];  // first forward tile index of position i (prefix sums)
+  int32_t P;
+};
+
+struct FwdArgs {
+  ShardTable st;
+  const void* H;
+  const int64_t* targets;
+  int64_t T;
+  int32_t d;
+  int32_t n_tok_blocks, n_splits, n_tiles;
+  float* m_part;  // [n_splits][T]
+  float* s_part;  // [n_splits][T]
+  float* y_tgt;   // [T]
+};
+
+struct CombArgs {
+  const float* m_part;
+  const float* s_part;
+  const float* y_tgt;
+  const int64_t* targets;
+  int64_t T, V, ignore_index;
+  int32_t n_splits;
+  float* loss;
+  float* lse;
+  unsigned long long* bad_counter;
+};
+
+struct GradArgs {
+  const void* W;   // first row of this vocabulary chunk, [M, d]
+  const void* H;   // whole H [T, d]
+  const int64_t* targets;
+  const float* lse;
+  const float* grad;
+  void* strip;     // [Vc][ldg]
+  int64_t ldg;
+  int64_t t0;      // first token of this chunk
+  int64_t gid0;    // global id of the chunk's first row
+  int64_t V, ignore_index;
+  int32_t M;       // vocabulary rows in this chunk
+  int32_t N;       // tokens in this chunk
+  int32_t d;
+  int32_t n_vt;    // vocabulary tiles over M
+};
+
+struct GemmArgs {
+  const void* A;
+  int64_t lda;
+  const void* B;
+  int64_t ldb;
+  float* C;
+  int64_t ldc;
+  int32_t M, N, K;
+  int32_t beta;
+  int32_t n_nt;  // filled by the launcher
+};
+
+struct TileShape {
+  int fwd_bm, fwd_bn, grad_bm, grad_bn;
+};
+
+TileShape tile_shape(int dtype);
+bool run_ws_init(unsigned long long* counter, hipStream_t s);
+bool run_fill_zero(float* p, int64_t n, hipStream_t s);
+bool run_fwd(int dtype, const FwdArgs& a, hipStream_t s);
+bool run_comb(const CombArgs& a, hipStream_t s);
+bool run_grad(int dtype, const GradArgs& a, hipStream_t s);
+bool run_count_bad(const int64_t* targets, int64_t T, int64_t V, int64_t ignore_index,
+                   unsigned long long* counter, hipStream_t s);
+bool run_dH(int dtype, const GemmArgs& a, hipStream_t s);
+bool run_dW(int dtype, const GemmArgs& a, hipStream_t s);
+
+}  // namespace vpce

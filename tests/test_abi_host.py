@@ -1,0 +1,143 @@
+"""Host-side tests of the C ABI (no GPU): the library loads, exports every symbol the
+header declares, and every argument / shape / order / alignment / workspace error
+is returned before any HIP call.  Workspace sizes do not depend on V."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2609_14306_amd as vp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "vpce.h")
+
+pytestmark = pytest.mark.skipif(not os.path.exists(vp.LIB_PATH),
+                                reason="libvpce.so not built (run __graft_entry__.build())")
+
+FAKE = 0x100000  # an aligned, never-dereferenced pointer value for validation tests
+
+
+def declared_functions():
+    src = open(HEADER).read()
+    return sorted(set(re.findall(r"^\s*(?:vp_status|const char\*|int)\s+(vp_\w+)\s*\(", src, re.M)))
+
+
+def test_header_declarations_match_binding():
+    assert declared_functions() == sorted(vp.EXPORTED)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = vp.load_library()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert vp.vp_abi_version() == 1
+
+
+def test_status_strings():
+    for s in range(10):
+        assert vp.vp_status_str(s)
+    assert vp.vp_status_str(0) == "ok"
+
+
+def _prob(**kw):
+    base = dict(T=4096, d=2880, shard_rows=[25136] * 8, dtype=vp.VP_BF16)
+    base.update(kw)
+    return vp.Problem(**base)
+
+
+def test_workspace_size_independent_of_V():
+    sizes = set()
+    for V in (32768, 65536, 131072, 201088, 262144):
+        rows = [V // 8] * 8
+        sizes.add(vp.vp_ce_workspace_size(_prob(T=32768, shard_rows=rows)))
+    assert len(sizes) == 1, sizes
+    fwd, bwd = sizes.pop()
+    assert 0 < fwd < 64 << 20 and 0 < bwd <= (256 << 20) + 4096
+
+
+def test_workspace_respects_strip_budget():
+    _, small = vp.vp_ce_workspace_size(_prob(strip_elems=1 << 20))
+    _, big = vp.vp_ce_workspace_size(_prob(strip_elems=1 << 26))
+    assert small < big and small <= (1 << 21) + 4096
+
+
+@pytest.mark.parametrize("kw,status", [
+    (dict(T=-1), vp.VP_ERR_SHAPE),
+    (dict(d=0), vp.VP_ERR_SHAPE),
+    (dict(d=12), vp.VP_ERR_SHAPE),
+    (dict(shard_rows=[]), vp.VP_ERR_SHAPE),
+    (dict(shard_rows=[1] * 65), vp.VP_ERR_SHAPE),
+    (dict(shard_rows=[0, 0]), vp.VP_ERR_SHAPE),
+    (dict(shard_rows=[5, -1]), vp.VP_ERR_SHAPE),
+    (dict(dtype=7), vp.VP_ERR_DTYPE),
+    (dict(shard_rows=[4, 4], order=[0, 0]), vp.VP_ERR_ORDER),
+    (dict(shard_rows=[4, 4], order=[0, 2]), vp.VP_ERR_ORDER),
+    (dict(strip_elems=-5), vp.VP_ERR_SHAPE),
+])
+def test_invalid_problem(kw, status):
+    with pytest.raises(vp.VpError) as e:
+        vp.vp_ce_workspace_size(_prob(**kw))
+    assert e.value.status == status
+
+
+def _fwd(prob, H=FAKE, W=(FAKE,), t=FAKE, loss=FAKE, lse=FAKE, ws=FAKE, ws_bytes=None):
+    lib = vp.load_library()
+    fwd_b, _ = vp.vp_ce_workspace_size(prob)
+    arr = (ctypes.c_void_p * max(len(W), 1))(*W)
+    return lib.vp_ce_forward(ctypes.byref(prob.c), H, arr, t, loss, lse, ws,
+                             fwd_b if ws_bytes is None else ws_bytes, 0)
+
+
+def _bwd(prob, H=FAKE, W=(FAKE,), t=FAKE, lse=FAKE, g=FAKE, dH=FAKE, dW=(FAKE,), ws=FAKE,
+         ws_bytes=None):
+    lib = vp.load_library()
+    _, bwd_b = vp.vp_ce_workspace_size(prob)
+    Wa = (ctypes.c_void_p * max(len(W), 1))(*W)
+    dWa = (ctypes.c_void_p * max(len(dW), 1))(*dW)
+    return lib.vp_ce_backward(ctypes.byref(prob.c), H, Wa, t, lse, g, dH, dWa, ws,
+                              bwd_b if ws_bytes is None else ws_bytes, 0)
+
+
+def test_forward_argument_errors_before_launch():
+    p = _prob(shard_rows=[100])
+    assert _fwd(p, ws=None) == vp.VP_ERR_WORKSPACE
+    assert _fwd(p, ws_bytes=16) == vp.VP_ERR_WORKSPACE
+    assert _fwd(p, ws=FAKE + 8) == vp.VP_ERR_ALIGN
+    assert _fwd(p, H=FAKE + 2) == vp.VP_ERR_ALIGN
+    assert _fwd(p, W=(FAKE + 4,)) == vp.VP_ERR_ALIGN
+    assert _fwd(p, W=(None,)) == vp.VP_ERR_NULL
+    assert _fwd(p, H=None) == vp.VP_ERR_NULL
+    assert _fwd(p, t=None) == vp.VP_ERR_NULL
+    assert _fwd(p, loss=None) == vp.VP_ERR_NULL
+    assert _fwd(p, lse=None) == vp.VP_ERR_NULL
+    lib = vp.load_library()
+    assert lib.vp_ce_forward(None, FAKE, None, FAKE, FAKE, FAKE, FAKE, 1 << 30, 0) == vp.VP_ERR_NULL
+    arr = (ctypes.c_void_p * 1)(FAKE)
+    assert lib.vp_ce_forward(ctypes.byref(p.c), FAKE, None, FAKE, FAKE, FAKE, FAKE, 1 << 30,
+                             0) == vp.VP_ERR_NULL
+    del arr
+
+
+def test_backward_argument_errors_before_launch():
+    p = _prob(shard_rows=[100, 0])
+    W = (FAKE, None)
+    dW = (FAKE, None)
+    assert _bwd(p, W=W, dW=dW, ws=None) == vp.VP_ERR_WORKSPACE
+    assert _bwd(p, W=W, dW=dW, ws_bytes=255) == vp.VP_ERR_WORKSPACE
+    assert _bwd(p, W=W, dW=(FAKE + 4, None)) == vp.VP_ERR_ALIGN
+    assert _bwd(p, W=W, dW=(None, None)) == vp.VP_ERR_NULL
+    assert _bwd(p, W=W, dW=dW, dH=None) == vp.VP_ERR_NULL
+    assert _bwd(p, W=W, dW=dW, lse=None) == vp.VP_ERR_NULL
+    assert _bwd(p, W=W, dW=dW, g=None) == vp.VP_ERR_NULL
+    assert _bwd(p, W=W, dW=dW, dH=FAKE + 4) == vp.VP_ERR_ALIGN
+    bad_order = _prob(shard_rows=[100, 0], order=[1, 1])
+    lib = vp.load_library()
+    Wa = (ctypes.c_void_p * 2)(*W)
+    assert lib.vp_ce_backward(ctypes.byref(bad_order.c), FAKE, Wa, FAKE, FAKE, FAKE, FAKE, Wa, FAKE,
+                              1 << 30, 0) == vp.VP_ERR_ORDER
+
+
+def test_check_null_workspace():
+    lib = vp.load_library()
+    assert lib.vp_ce_check(None, None, None) == vp.VP_ERR_NULL

@@ -1,0 +1,173 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle on the
+same seeded inputs (element by element for loss and lse, relative Frobenius for
+dH and dW), at sizes the oracle finishes in seconds that span several tiles and
+ragged tails, plus the reduced-token versions of the four bf16 workloads at their
+full d, V and shard layout."""
+import numpy as np
+import pytest
+
+import workloads as wl
+from helpers import compare_all, run_gpu, run_oracle
+
+pytestmark = pytest.mark.gpu
+
+
+def _case(name, **kw):
+    return wl.make_inputs(name, **kw)
+
+
+def test_tiny_f32_full_workload():
+    inp = _case("tiny_f32_T256_d256_V2048_P8")
+    g = wl.random_grad_loss(inp.T, 0, "mean", inp.targets)
+    got = run_gpu(inp, g)
+    ref = run_oracle(inp, g)
+    compare_all(inp, got, ref, "tiny f32")
+    assert got["bad_fwd"] == 0 and got["bad_bwd"] == 0
+
+
+@pytest.mark.parametrize("dtype_name", ["tiny_f32_T256_d256_V2048_P8", "bf16_T4096_d2880_V201088_P8"])
+def test_ragged_shards_and_tiles(dtype_name):
+    # T, d and every shard length off the tile grid; an empty shard; a permuted order.
+    inp = _case(dtype_name, T=333, d=200, V=1100, P=1, seed=3)
+    inp = wl.resplit(inp, [100, 0, 257, 131, 612], order=[3, 0, 4, 1, 2])
+    g = wl.random_grad_loss(inp.T, 3, "random")
+    got = run_gpu(inp, g)
+    ref = run_oracle(inp, g)
+    compare_all(inp, got, ref, f"ragged {inp.dtype}")
+
+
+@pytest.mark.parametrize("name", [w.name for w in wl.WORKLOAD_LIST[1:]])
+def test_full_shape_reduced_tokens(name):
+    # Full d, V, shard layout, order, target law and logit scale; 300 tokens.
+    inp = _case(name, T=300)
+    g = wl.random_grad_loss(inp.T, 1, "random")
+    got = run_gpu(inp, g)
+    ref = run_oracle(inp, g)
+    errs = compare_all(inp, got, ref, name)
+    print(name, errs, "max|logit|", ref["max_abs_logit"])
+
+
+def test_small_strip_forces_many_chunks():
+    inp = _case("bf16_T4096_d2880_V201088_P8", T=700, d=256, V=3000, P=3, seed=5)
+    g = wl.random_grad_loss(inp.T, 5, "sum")
+    ref = run_oracle(inp, g)
+    got = run_gpu(inp, g, strip_elems=128 * 256)  # 256-token by 128-row strip
+    compare_all(inp, got, ref, "small strip")
+    got2 = run_gpu(inp, g)
+    compare_all(inp, got2, ref, "default strip")
+
+
+def test_edge_targets_and_degenerate_cases():
+    inp = _case("bf16_T4096_d2880_V201088_P8", T=130, d=64, V=600, P=1, seed=7)
+    inp = wl.resplit(inp, [128, 128, 344], order=[2, 1, 0])
+    t = inp.targets.copy()
+    t[:8] = [0, 599, 127, 128, 255, 256, -100, 343]
+    t[8:12] = -100
+    inp.targets[:] = t
+    g = wl.random_grad_loss(inp.T, 7, "random")
+    got = run_gpu(inp, g)
+    ref = run_oracle(inp, g)
+    compare_all(inp, got, ref, "edge targets")
+
+
+def test_single_token_single_shard():
+    inp = _case("tiny_f32_T256_d256_V2048_P8", T=1, d=8, V=5, P=1, seed=11)
+    g = np.ones(1, dtype=np.float32)
+    got = run_gpu(inp, g)
+    ref = run_oracle(inp, g)
+    compare_all(inp, got, ref, "T=1")
+
+
+def test_all_targets_ignored():
+    inp = _case("bf16_T4096_d2880_V201088_P8", T=64, d=32, V=300, P=2, seed=13)
+    inp.targets[:] = -100
+    g = wl.random_grad_loss(inp.T, 13, "mean", inp.targets)  # N_valid = 0 -> g = 0
+    got = run_gpu(inp, g)
+    ref = run_oracle(inp, g)
+    assert np.all(got["loss"] == 0.0) and np.all(got["dH"] == 0.0)
+    assert all(np.all(w == 0.0) for w in got["dW_shards"])
+    compare_all(inp, got, ref, "all ignored")
+
+
+def test_out_of_range_target_is_reported():
+    inp = _case("tiny_f32_T256_d256_V2048_P8", T=40, d=16, V=100, P=2, seed=17)
+    inp.targets[5] = 100
+    inp.targets[9] = -3
+    g = wl.random_grad_loss(inp.T, 17, "sum")
+    got = run_gpu(inp, g)
+    assert got["bad_fwd"] == 2 and got["bad_bwd"] == 2
+    assert np.isnan(got["loss"][5]) and np.isnan(got["loss"][9])
+    ok = np.ones(inp.T, bool)
+    ok[[5, 9]] = False
+    assert np.all(np.isfinite(got["loss"][ok])) and np.all(np.isfinite(got["lse"]))
+    assert np.all(np.isnan(got["dH"][5]))
+
+
+def test_empty_token_batch():
+    import torch
+
+    import paper_2609_14306_amd as vp
+    inp = _case("bf16_T4096_d2880_V201088_P8", T=0, d=16, V=50, P=2, seed=19)
+    from helpers import to_device
+    H, Ws, t = to_device(inp)
+    loss, lse = vp.forward(H, Ws, t)
+    assert loss.numel() == 0
+    dW = [torch.full((w.shape[0], 16), 7.0, device="cuda") for w in Ws]
+    dH, dW = vp.backward(H, Ws, t, lse, torch.empty(0, device="cuda"), dW_shards=dW)
+    torch.cuda.synchronize()
+    assert all(float(w.abs().max()) == 0.0 for w in dW)
+    dW2 = [torch.full((w.shape[0], 16), 7.0, device="cuda") for w in Ws]
+    vp.backward(H, Ws, t, lse, torch.empty(0, device="cuda"), dW_shards=dW2, accumulate=True)
+    torch.cuda.synchronize()
+    assert all(float((w - 7.0).abs().max()) == 0.0 for w in dW2)
+
+
+def test_accumulate_dw_adds_rank_contributions():
+    # Two "ranks" with distinct batches meet the same shard; dW accumulates both.
+    import torch
+
+    import paper_2609_14306_amd as vp
+    from helpers import assert_grad_close, oracle_inputs, to_device
+    import oracle
+    a = _case("bf16_T4096_d2880_V201088_P8", T=150, d=96, V=700, P=2, seed=23)
+    b = _case("bf16_T4096_d2880_V201088_P8", T=90, d=96, V=700, P=2, seed=24)
+    b = wl.resplit(b, a.shard_rows)
+    b.W_shards = a.W_shards
+    ga = wl.random_grad_loss(a.T, 1, "random")
+    gb = wl.random_grad_loss(b.T, 2, "random")
+    Ha, Ws, ta = to_device(a)
+    Hb, _, tb = to_device(b)
+    _, lse_a = vp.forward(Ha, Ws, ta)
+    _, lse_b = vp.forward(Hb, Ws, tb)
+    _, dW = vp.backward(Ha, Ws, ta, lse_a, torch.from_numpy(ga).cuda())
+    vp.backward(Hb, Ws, tb, lse_b, torch.from_numpy(gb).cuda(), dW_shards=dW, accumulate=True)
+    torch.cuda.synchronize()
+    got = np.concatenate([w.cpu().numpy() for w in dW])
+    Ha64, W64 = oracle_inputs(a)
+    Hb64, _ = oracle_inputs(b)
+    ra = oracle.forward_backward(Ha64, W64, a.targets, ga)
+    rb = oracle.forward_backward(Hb64, W64, b.targets, gb)
+    assert_grad_close("bf16", got, ra["dW"] + rb["dW"], "accumulated dW")
+
+
+def test_order_invariance_and_determinism():
+    inp = _case("longctx_bf16_T32768_d2880_V201088_P8_ring", T=512, d=384, V=20000, seed=29)
+    g = wl.random_grad_loss(inp.T, 29, "random")
+    a = run_gpu(inp, g)
+    b = run_gpu(inp, g)
+    for k in ("loss", "lse", "dH"):
+        assert np.array_equal(a[k], b[k]), f"{k} not bitwise reproducible"
+    for x, y in zip(a["dW_shards"], b["dW_shards"]):
+        assert np.array_equal(x, y)
+    r = run_gpu(inp, g, order=list(reversed(inp.order)))
+    rel = np.abs(r["lse"] - a["lse"]) / np.abs(a["lse"])
+    assert rel.max() <= 1e-6, rel.max()
+    # Rows of G sum to zero, so sum_v dW_v = 0 up to the bf16 rounding of G: with unit
+    # roundoff u = 2^-8, |sum_v G^_tv| <= u * sum_v |G_tv| = 2u g_t (1 - p_t) <= 2u g_t,
+    # hence ||sum_v dW_v|| <= 2u sum_t g_t ||h_t|| (plus float32 accumulation slack).
+    dW = np.concatenate(a["dW_shards"]).astype(np.float64)
+    from helpers import oracle_inputs
+    H64, _ = oracle_inputs(inp)
+    live = inp.targets != inp.ignore_index
+    bound = (2 * 2.0 ** -8 + 1e-4) * float(np.sum(g[live] * np.linalg.norm(H64[live], axis=1)))
+    assert np.linalg.norm(dW.sum(axis=0)) <= bound

@@ -192,6 +192,16 @@ def make_inputs(w: Workload | str, T: Optional[int] = None, V: Optional[int] = N
     return Inputs(w, T, d, V, w.dtype, H, W_shards, targets, visiting_order(w.order, P), rows)
 
 
+def resplit(inp: Inputs, rows: Sequence[int], order: Optional[Sequence[int]] = None) -> Inputs:
+    """The same vocabulary projection split into shards of the given row counts."""
+    W = np.concatenate(inp.W_shards, axis=0)
+    assert sum(rows) == W.shape[0]
+    offs = np.cumsum([0] + list(rows))
+    shards = [np.ascontiguousarray(W[offs[p]:offs[p + 1]]) for p in range(len(rows))]
+    order = list(range(len(rows))) if order is None else list(order)
+    return dataclasses.replace(inp, W_shards=shards, shard_rows=list(rows), order=order)
+
+
 def random_grad_loss(T: int, seed: int, kind: str = "mean", targets: Optional[np.ndarray] = None,
                      ignore_index: int = IGNORE_INDEX) -> np.ndarray:
     """Upstream per-token gradient g [T] (float32): 'mean' (1/N_valid), 'sum' (1) or 'random'."""
