@@ -81,14 +81,16 @@ typedef struct {
   const int32_t* order;       /* host [P]: visiting order, a permutation of 0..P-1; NULL = 0..P-1 */
   int64_t ignore_index;       /* target value that marks a token without loss (e.g. -100) */
   uint32_t flags;             /* VP_ACCUMULATE_DW */
-  int64_t strip_elems;        /* backward residual-strip budget in elements; 0 = default (64 Mi) */
+  int64_t strip_elems;        /* backward residual-strip budget in elements per layout,
+                                 0..2^30; 0 = default (64 Mi) */
 } vp_problem;
 
 /* Workspace sizes in bytes for vp_ce_forward (*fwd_bytes) and vp_ce_backward
  * (*bwd_bytes); either output pointer may be NULL.  Host only, needs no device.
  * forward: per-token partial states of the vocabulary splits, O(T);
- * backward: the residual strip (at most strip_elems elements), independent of T
- * beyond that budget and of V. */
+ * backward: the residual strip in two layouts (2 x strip_elems elements at
+ * most), H^T (T x d elements) and W^T of one vocabulary chunk (d x strip
+ * columns).  Neither depends on V. */
 vp_status vp_ce_workspace_size(const vp_problem* prob, size_t* fwd_bytes, size_t* bwd_bytes);
 
 /* Forward (Sec. 3.2, Eq. of the online-softmax fold; Algorithm 2):

@@ -14,7 +14,7 @@
 namespace {
 
 constexpr size_t kHeaderBytes = 256;       // error counter + reserved
-constexpr int64_t kDefaultStrip = 64ll << 20;  // residual-strip budget in elements
+constexpr int64_t kDefaultStrip = 100ll << 20;  // residual-strip budget in elements per layout
 constexpr int kTargetGroups = 512;         // forward workgroups to aim for (2 per CU on 256 CUs)
 constexpr int kMaxSplits = 32;
 
@@ -32,7 +32,7 @@ vp_status validate(const vp_problem* p, int64_t* V_out) {
   if (p->T > (1ll << 30)) return VP_ERR_SHAPE;
   if (p->P < 1 || p->P > VP_MAX_SHARDS) return VP_ERR_SHAPE;
   if (!p->shard_rows) return VP_ERR_NULL;
-  if (p->strip_elems < 0) return VP_ERR_SHAPE;
+  if (p->strip_elems < 0 || p->strip_elems > (1ll << 30)) return VP_ERR_SHAPE;
   int64_t V = 0;
   for (int i = 0; i < p->P; ++i) {
     if (p->shard_rows[i] < 0 || p->shard_rows[i] > (1ll << 30)) return VP_ERR_SHAPE;
@@ -65,31 +65,40 @@ size_t fwd_ws_bytes(const vp_problem* p) {
   return kHeaderBytes + 2 * align256(S * T * 4) + align256(T * 4);
 }
 
-// Backward strip plan: Tc tokens by Vc vocabulary rows, Tc*Vc <= budget,
-// as square as the token count allows (this minimises the float32
+// Backward plan.  The softmax residual of a strip of Tc tokens by Vc
+// vocabulary rows is staged in both layouts (G [Vc][Tc] and G^T [Tc][Vc]);
+// Tc*Vc <= budget, as square as the token count allows (the float32
 // read-modify-write traffic of dH across vocabulary chunks plus that of dW
-// across token chunks, which is proportional to 1/Vc + 1/Tc).
+// across token chunks is proportional to 1/Vc + 1/Tc).  The workspace also
+// holds H^T [d][T_pad] (written once per call) and W^T [d][Vc] of the current
+// vocabulary chunk.  Nothing here depends on V.
 struct StripPlan {
-  int64_t Tc, Vc, ldg;
+  int64_t Tc, Vc, T_pad;
+  size_t off_g, off_gt, off_ht, off_wt, total;
 };
 
 StripPlan strip_plan(const vp_problem* p) {
   const vpce::TileShape ts = vpce::tile_shape(p->dtype);
   const int64_t budget = p->strip_elems > 0 ? p->strip_elems : kDefaultStrip;
-  const int64_t Tpad = round_up(std::max<int64_t>(p->T, 1), ts.grad_bn);
-  const int64_t side = round_down((int64_t)std::sqrt((double)budget), ts.grad_bn);
+  const int64_t T = std::max<int64_t>(p->T, 1);
+  const int64_t side = std::max<int64_t>(ts.grad_bn, round_down((int64_t)std::sqrt((double)budget), ts.grad_bn));
   StripPlan s;
-  s.Tc = std::max<int64_t>(ts.grad_bn, std::min<int64_t>(Tpad, side));
-  s.ldg = s.Tc;
+  // Tokens: ceil(T / side) balanced, tile-aligned chunks; vocabulary rows: the
+  // rest of the budget, tile-aligned.
+  s.Tc = std::min<int64_t>(round_up(T, ts.grad_bn), round_up(ceil_div(T, ceil_div(T, side)), ts.grad_bn));
   s.Vc = std::max<int64_t>(ts.grad_bm, std::min<int64_t>(round_down(budget / s.Tc, ts.grad_bm),
-                                                        1ll << 20));
+                                                        32768));
+  s.T_pad = round_up(std::max<int64_t>(p->T, 1), 256);
+  const size_t eb = elem_bytes(p->dtype);
+  s.off_g = kHeaderBytes;
+  s.off_gt = s.off_g + align256((size_t)s.Vc * s.Tc * eb);
+  s.off_ht = s.off_gt + align256((size_t)s.Tc * s.Vc * eb);
+  s.off_wt = s.off_ht + align256((size_t)p->d * s.T_pad * eb);
+  s.total = s.off_wt + align256((size_t)p->d * s.Vc * eb);
   return s;
 }
 
-size_t bwd_ws_bytes(const vp_problem* p) {
-  const StripPlan s = strip_plan(p);
-  return kHeaderBytes + align256((size_t)s.Vc * (size_t)s.ldg * elem_bytes(p->dtype));
-}
+size_t bwd_ws_bytes(const vp_problem* p) { return strip_plan(p).total; }
 
 void build_table(const vp_problem* p, const void* const* W_shards, int bm, vpce::ShardTable* st,
                  int32_t* n_tiles) {
@@ -247,8 +256,24 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
 
   const vpce::TileShape ts = vpce::tile_shape(prob->dtype);
   const StripPlan plan = strip_plan(prob);
-  void* strip = (char*)ws + kHeaderBytes;
+  char* wsb = (char*)ws;
+  void* strip = wsb + plan.off_g;
+  void* strip_t = wsb + plan.off_gt;
+  void* Ht = wsb + plan.off_ht;
+  void* Wt = wsb + plan.off_wt;
   const size_t eb = elem_bytes(prob->dtype);
+
+  {  // H^T [d][T_pad], zero beyond T
+    vpce::TransposeArgs tr;
+    tr.in = H;
+    tr.ld_in = d;
+    tr.out = Ht;
+    tr.ld_out = plan.T_pad;
+    tr.R = (int32_t)T;
+    tr.C = (int32_t)d;
+    tr.R_pad = (int32_t)plan.T_pad;
+    if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
+  }
 
   int64_t off[VP_MAX_SHARDS];
   int64_t acc = 0;
@@ -256,16 +281,33 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
     off[q] = acc;
     acc += prob->shard_rows[q];
   }
+  // Balanced chunks: a shard of Vq rows is cut into ceil(Vq / Vc) chunks of equal
+  // tile-aligned size (never above the planned Vc), the tokens likewise.
+  const int64_t tc = plan.Tc;
   bool first_vchunk = true;
   for (int i = 0; i < prob->P; ++i) {
     const int q = prob->order ? prob->order[i] : i;
     const int64_t Vq = prob->shard_rows[q];
-    for (int64_t v0 = 0; v0 < Vq; v0 += plan.Vc) {
-      const int64_t M = std::min<int64_t>(plan.Vc, Vq - v0);
+    if (Vq == 0) continue;
+    const int64_t vc = std::min<int64_t>(
+        plan.Vc, round_up(ceil_div(Vq, ceil_div(Vq, plan.Vc)), ts.grad_bm));
+    for (int64_t v0 = 0; v0 < Vq; v0 += vc) {
+      const int64_t M = std::min<int64_t>(vc, Vq - v0);
       const char* Wc = (const char*)W_shards[q] + (size_t)v0 * d * eb;
       float* dWc = dW_shards[q] + v0 * d;
-      for (int64_t t0 = 0; t0 < T; t0 += plan.Tc) {
-        const int64_t N = std::min<int64_t>(plan.Tc, T - t0);
+      {  // W^T of this chunk, [d][Vc], zero beyond M
+        vpce::TransposeArgs tr;
+        tr.in = Wc;
+        tr.ld_in = d;
+        tr.out = Wt;
+        tr.ld_out = plan.Vc;
+        tr.R = (int32_t)M;
+        tr.C = (int32_t)d;
+        tr.R_pad = (int32_t)round_up(M, 8);
+        if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
+      }
+      for (int64_t t0 = 0; t0 < T; t0 += tc) {
+        const int64_t N = std::min<int64_t>(tc, T - t0);
         vpce::GradArgs g;
         g.W = Wc;
         g.H = H;
@@ -273,7 +315,9 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
         g.lse = lse;
         g.grad = grad_loss;
         g.strip = strip;
-        g.ldg = plan.ldg;
+        g.strip_t = strip_t;
+        g.ldg = plan.Tc;
+        g.ldgt = plan.Vc;
         g.t0 = t0;
         g.gid0 = off[q] + v0;
         g.V = V;
@@ -284,33 +328,30 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
         g.n_vt = (int32_t)ceil_div(M, ts.grad_bm);
         if (!vpce::run_grad(prob->dtype, g, s)) return VP_ERR_HIP;
 
-        vpce::GemmArgs h;  // dH[t0 : t0+N] (+)= G^T W_chunk
-        h.A = strip;
-        h.lda = plan.ldg;
-        h.B = Wc;
-        h.ldb = d;
+        vpce::GemmArgs h;  // dH[t0 : t0+N] (+)= G^T W_chunk = G^T . (W^T)^T
+        h.A = strip_t;
+        h.lda = plan.Vc;
+        h.B = Wt;
+        h.ldb = plan.Vc;
         h.C = dH + t0 * d;
         h.ldc = d;
         h.M = (int32_t)N;
         h.N = (int32_t)d;
         h.K = (int32_t)M;
         h.beta = first_vchunk ? 0 : 1;
-        h.n_nt = 0;
-        if (!vpce::run_dH(prob->dtype, h, s)) return VP_ERR_HIP;
 
-        vpce::GemmArgs w;  // dW_chunk (+)= G H[t0 : t0+N]
+        vpce::GemmArgs w;  // dW_chunk (+)= G H[t0 : t0+N] = G . (H^T)^T
         w.A = strip;
-        w.lda = plan.ldg;
-        w.B = (const char*)H + (size_t)t0 * d * eb;
-        w.ldb = d;
+        w.lda = plan.Tc;
+        w.B = (const char*)Ht + (size_t)t0 * eb;
+        w.ldb = plan.T_pad;
         w.C = dWc;
         w.ldc = d;
         w.M = (int32_t)M;
         w.N = (int32_t)d;
         w.K = (int32_t)N;
         w.beta = (t0 > 0 || accumulate) ? 1 : 0;
-        w.n_nt = 0;
-        if (!vpce::run_dW(prob->dtype, w, s)) return VP_ERR_HIP;
+        if (!vpce::run_gemm_pair(prob->dtype, h, w, s)) return VP_ERR_HIP;
       }
       first_vchunk = false;
     }

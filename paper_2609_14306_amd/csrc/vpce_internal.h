@@ -48,8 +48,9 @@ struct GradArgs {
   const int64_t* targets;
   const float* lse;
   const float* grad;
-  void* strip;     // [Vc][ldg]
-  int64_t ldg;
+  void* strip;     // G   [Vc][ldg]  (token columns contiguous)
+  void* strip_t;   // G^T [Tc][ldgt] (vocabulary columns contiguous)
+  int64_t ldg, ldgt;
   int64_t t0;      // first token of this chunk
   int64_t gid0;    // global id of the chunk's first row
   int64_t V, ignore_index;
@@ -59,6 +60,8 @@ struct GradArgs {
   int32_t n_vt;    // vocabulary tiles over M
 };
 
+// C[M][N] = (beta ? C : 0) + A B^T with A [M][K] (row stride lda) and B [N][K]
+// (row stride ldb), both k-contiguous.
 struct GemmArgs {
   const void* A;
   int64_t lda;
@@ -68,7 +71,15 @@ struct GemmArgs {
   int64_t ldc;
   int32_t M, N, K;
   int32_t beta;
-  int32_t n_nt;  // filled by the launcher
+};
+
+// out[c][r] = in[r][c] for r < R, c < C; out[c][r] = 0 for R <= r < R_pad.
+struct TransposeArgs {
+  const void* in;
+  int64_t ld_in;
+  void* out;
+  int64_t ld_out;
+  int32_t R, C, R_pad;
 };
 
 struct TileShape {
@@ -83,7 +94,8 @@ bool run_comb(const CombArgs& a, hipStream_t s);
 bool run_grad(int dtype, const GradArgs& a, hipStream_t s);
 bool run_count_bad(const int64_t* targets, int64_t T, int64_t V, int64_t ignore_index,
                    unsigned long long* counter, hipStream_t s);
-bool run_dH(int dtype, const GemmArgs& a, hipStream_t s);
-bool run_dW(int dtype, const GemmArgs& a, hipStream_t s);
+// Two independent GEMMs (the dH and dW contractions of one strip) in one launch.
+bool run_gemm_pair(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t s);
+bool run_transpose(int dtype, const TransposeArgs& a, hipStream_t s);
 
 }  // namespace vpce

@@ -2,11 +2,19 @@
 // cross-entropy, forward with an online log-sum-exp fold and backward with
 // logits recompute (arXiv 2609.14306, Sec. 3.2 and the appendix on Ring-DTP).
 //
-// One MFMA GEMM mainloop serves the four contractions of the path:
-//   logits (forward and recompute)  C[v][t] = sum_k W[v][k] H[t][k]   (both K-major)
-//   dH                              C[t][n] = sum_v G[v][t] W[v][n]   (both MN-major)
-//   dW                              C[v][n] = sum_t G[v][t] H[t][n]   (A K-major, B MN-major)
-// The residual strip G is stored vocabulary-row by token-column ([Vc][ldg]).
+// One MFMA GEMM mainloop, C[m][n] = sum_k A[m][k] B[n][k] with both operands
+// k-contiguous, serves the four contractions of the path:
+//   logits (forward and recompute)  C[v][t] = sum_k W[v][k]   H[t][k]
+//   dH                              C[t][n] = sum_v G^T[t][v] W^T[n][v]
+//   dW                              C[v][n] = sum_t G[v][t]   H^T[n][t]
+// The backward stores the softmax residual of a (vocabulary chunk, token
+// chunk) strip in both layouts (G and G^T) and uses transposed copies of H
+// (once per call) and of each vocabulary chunk of W, so that every operand is
+// staged k-contiguous and every MFMA fragment is one 16-byte LDS read (on
+// gfx950 the LDS transpose read sustains well under half the bandwidth of a
+// plain 16-byte read, and transposing in registers costs VALU work and LDS
+// bank conflicts).
+//
 // Logits are computed transposed (vocabulary rows, token columns) so that in the
 // MFMA accumulator layout every lane owns whole token columns: the online
 // softmax state of a token lives in one lane's registers and needs no
@@ -19,21 +27,18 @@
 namespace vpce {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
-typedef short s16x4_t __attribute__((ext_vector_type(4)));
 typedef float f32x16_t __attribute__((ext_vector_type(16)));
-typedef short __attribute__((address_space(3))) * lds_s16_ptr;
 
-constexpr int kThreads = 256;  // 4 wavefronts of 64, arranged 2 x 2 over the tile
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 // ---------------------------------------------------------------------------
 // Element policies.  BK: k elements staged per LDS pass (128 bytes per row);
-// KSTEP: k consumed by one MFMA; VEC: elements per 16-byte global load.
+// KSTEP: k consumed by one MFMA; VEC: elements per 16 bytes.
 struct Bf16 {
   using storage = uint16_t;
   using frag = bf16x8_t;
-  static constexpr int BK = 64, KSTEP = 16, VEC = 8, PADK = 8, PADM = 16;
+  static constexpr int BK = 64, KSTEP = 16, VEC = 8, PADK = 8;
   __device__ static f32x16_t mma(frag a, frag b, f32x16_t c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
@@ -46,7 +51,7 @@ struct Bf16 {
 struct F32 {
   using storage = float;
   using frag = float;
-  static constexpr int BK = 32, KSTEP = 2, VEC = 4, PADK = 4, PADM = 4;
+  static constexpr int BK = 32, KSTEP = 2, VEC = 4, PADK = 4;
   __device__ static f32x16_t mma(frag a, frag b, f32x16_t c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
   }
@@ -54,53 +59,39 @@ struct F32 {
 };
 
 // ---------------------------------------------------------------------------
-// Global -> register -> LDS staging of one operand tile.  ROWS is the extent of
-// the operand's non-contracted dimension in the tile.  A K-major operand holds
-// element (r, k) at p[r * ld + k]; an MN-major one at p[k * ld + r].
-// Rows at or beyond R are clamped (K-major) or zero (MN-major): they only feed
-// accumulator rows/columns that are never stored.  k at or beyond K is zero,
-// so ragged contractions add nothing.
-template <class E, int ROWS, bool KMAJOR>
+// Global -> register -> LDS staging of one k-contiguous operand tile of ROWS x
+// BK (element (r, k) at p[r * ld + k]), written to LDS as [ROWS][BK + PADK].
+// Rows at or beyond R are clamped to R-1 (they only feed accumulator rows or
+// columns that are never stored); k at or beyond K reads as zero, so ragged
+// contractions add nothing.  K is checked per 16-byte chunk: an operand whose
+// K is not a multiple of VEC must hold finite values up to the next multiple.
+template <class E, int ROWS, int NT>
 struct Stage {
   using S = typename E::storage;
   static constexpr int BK = E::BK, VEC = E::VEC;
-  static constexpr int CHUNKS = ROWS * BK / VEC;
-  static constexpr int PER_THREAD = CHUNKS / kThreads;
-  static_assert(CHUNKS % kThreads == 0, "tile must split evenly over the workgroup");
-  static constexpr int LD = KMAJOR ? (BK + E::PADK) : (ROWS + E::PADM);
-  static constexpr int LDS_ELEMS = KMAJOR ? ROWS * LD : BK * LD;
-  uint4 regs[PER_THREAD];
+  static constexpr int LD = BK + E::PADK;
+  static constexpr int LDS_ELEMS = ROWS * LD;
+  static constexpr int UNITS = ROWS * BK / VEC;
+  static constexpr int PER = (UNITS + NT - 1) / NT;
+  uint4 regs[PER];
 
   __device__ __forceinline__ void load(const S* __restrict__ p, int64_t ld, int r0, int R, int k0,
                                        int K, int tid) {
 #pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = tid + i * kThreads;
-      if constexpr (KMAJOR) {
-        const int r = c / (BK / VEC), kc = (c % (BK / VEC)) * VEC;
-        const int rr = min(r0 + r, R - 1);
-        const int kk = k0 + kc;
-        regs[i] = (kk < K && rr >= 0) ? *(const uint4*)(p + (int64_t)rr * ld + kk)
-                                      : make_uint4(0, 0, 0, 0);
-      } else {
-        const int kr = c / (ROWS / VEC), rc = (c % (ROWS / VEC)) * VEC;
-        const int kk = k0 + kr, rr = r0 + rc;
-        regs[i] = (kk < K && rr < R) ? *(const uint4*)(p + (int64_t)kk * ld + rr)
-                                     : make_uint4(0, 0, 0, 0);
-      }
+    for (int i = 0; i < PER; ++i) {
+      const int u = tid + i * NT;
+      const int r = u / (BK / VEC), kc = (u % (BK / VEC)) * VEC;
+      const int rr = min(r0 + r, R - 1);
+      const int kk = k0 + kc;
+      regs[i] = (u < UNITS && kk < K && rr >= 0) ? *(const uint4*)(p + (int64_t)rr * ld + kk)
+                                                 : make_uint4(0, 0, 0, 0);
     }
   }
   __device__ __forceinline__ void store(S* lds, int tid) const {
 #pragma unroll
-    for (int i = 0; i < PER_THREAD; ++i) {
-      const int c = tid + i * kThreads;
-      int off;
-      if constexpr (KMAJOR) {
-        off = (c / (BK / VEC)) * LD + (c % (BK / VEC)) * VEC;
-      } else {
-        off = (c / (ROWS / VEC)) * LD + (c % (ROWS / VEC)) * VEC;
-      }
-      *(uint4*)(lds + off) = regs[i];
+    for (int i = 0; i < PER; ++i) {
+      const int u = tid + i * NT;
+      if (u < UNITS) *(uint4*)(lds + (u / (BK / VEC)) * LD + (u % (BK / VEC)) * VEC) = regs[i];
     }
   }
 };
@@ -109,32 +100,13 @@ struct Stage {
 // operand's non-contracted dimension) at k offset kbase of the staged tile.
 // 32x32x16 bf16: lane l takes row l%32 and k = kbase + 8*(l/32) + 0..7.
 // 32x32x2 f32:   lane l takes row l%32 and k = kbase + l/32.
-template <class E, int LD, bool KMAJOR>
+template <class E, int LD>
 __device__ __forceinline__ typename E::frag read_frag(const typename E::storage* lds, int row0,
                                                       int kbase, int lane) {
   if constexpr (sizeof(typename E::storage) == 2) {
-    if constexpr (KMAJOR) {
-      return *(const bf16x8_t*)(lds + (row0 + (lane & 31)) * LD + kbase + 8 * (lane >> 5));
-    } else {
-      // LDS transpose read: within each 16-lane group, lane 4b+c points at k-row b,
-      // columns 4c..4c+3; lane j of the group receives column j of the 4 k-rows.
-      const int g = lane >> 4, i = lane & 15;
-      const int krow = kbase + 8 * (g >> 1) + (i >> 2);
-      const int col = row0 + 16 * (g & 1) + 4 * (i & 3);
-      const typename E::storage* p0 = lds + krow * LD + col;
-      s16x4_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((s16x4_t __attribute__((address_space(3)))*)(p0));
-      s16x4_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
-          (s16x4_t __attribute__((address_space(3)))*)(p0 + 4 * LD));
-      typedef short s16x8_t __attribute__((ext_vector_type(8)));
-      s16x8_t v = __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7);
-      return __builtin_bit_cast(bf16x8_t, v);
-    }
+    return *(const bf16x8_t*)(lds + (row0 + (lane & 31)) * LD + kbase + 8 * (lane >> 5));
   } else {
-    if constexpr (KMAJOR) {
-      return lds[(row0 + (lane & 31)) * LD + kbase + (lane >> 5)];
-    } else {
-      return lds[(kbase + (lane >> 5)) * LD + row0 + (lane & 31)];
-    }
+    return lds[(row0 + (lane & 31)) * LD + kbase + (lane >> 5)];
   }
 }
 
@@ -142,29 +114,37 @@ __device__ __forceinline__ typename E::frag read_frag(const typename E::storage*
 // row 8*(r/4) + 4*(l/32) + r%4 and column l%32.
 __device__ __forceinline__ int acc_row(int r, int lane) { return 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3); }
 
-// Tile GEMM: acc += A[m0 : m0+BM, 0:K] * B[0:K, n0 : n0+BN] on a 2x2 grid of waves.
-template <class E, int BM, int BN, bool AK, bool BKM>
+// Tile GEMM: acc += A[m0 : m0+BM, 0:K] * B[n0 : n0+BN, 0:K]^T on a WGM x WGN grid of
+// wavefronts.  Two LDS buffers: while the waves multiply out of one, the next
+// k-slice (already fetched into registers one slice ahead) is written into the
+// other, so each k-slice costs a single workgroup barrier.
+template <class E, int BM_, int BN_, int WGM_, int WGN_>
 struct Gemm {
   using S = typename E::storage;
-  static constexpr int WM = BM / 2, WN = BN / 2, MB = WM / 32, NB = WN / 32;
-  using SA = Stage<E, BM, AK>;
-  using SB = Stage<E, BN, BKM>;
-  static constexpr int LDS_ELEMS = SA::LDS_ELEMS + SB::LDS_ELEMS;
+  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
+  static constexpr int NT = 64 * WGM * WGN;
+  static constexpr int WM = BM / WGM, WN = BN / WGN, MB = WM / 32, NB = WN / 32;
+  static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be whole 32x32 blocks");
+  using SA = Stage<E, BM, NT>;
+  using SB = Stage<E, BN, NT>;
+  static constexpr int BUF_ELEMS = SA::LDS_ELEMS + SB::LDS_ELEMS;
+  static constexpr int LDS_ELEMS = 2 * BUF_ELEMS;
+
+  __device__ __forceinline__ static int wave_m(int wave) { return (wave / WGN) * WM; }
+  __device__ __forceinline__ static int wave_n(int wave) { return (wave % WGN) * WN; }
 
   __device__ __forceinline__ static void run(f32x16_t (&acc)[MB][NB], const S* __restrict__ A,
                                              int64_t lda, int m0, int M, const S* __restrict__ B,
                                              int64_t ldb, int n0, int N, int K, S* smem) {
-    S* sA = smem;
-    S* sB = smem + SA::LDS_ELEMS;
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    const int wm = (wave >> 1) * WM, wn = (wave & 1) * WN;
+    const int wm = wave_m(wave), wn = wave_n(wave);
     SA la;
     SB lb;
     const int nk = (K + E::BK - 1) / E::BK;
     la.load(A, lda, m0, M, 0, K, tid);
     lb.load(B, ldb, n0, N, 0, K, tid);
-    la.store(sA, tid);
-    lb.store(sB, tid);
+    la.store(smem, tid);
+    lb.store(smem + SA::LDS_ELEMS, tid);
     __syncthreads();
     for (int kt = 0; kt < nk; ++kt) {
       const bool more = kt + 1 < nk;
@@ -172,27 +152,65 @@ struct Gemm {
         la.load(A, lda, m0, M, (kt + 1) * E::BK, K, tid);
         lb.load(B, ldb, n0, N, (kt + 1) * E::BK, K, tid);
       }
+      const S* sA = smem + (kt & 1) * BUF_ELEMS;
+      const S* sB = sA + SA::LDS_ELEMS;
+      // Fragments of sub-step kk+1 are read while the MFMAs of sub-step kk run.
+      constexpr int NKK = E::BK / E::KSTEP;
+      typename E::frag a[2][MB], b[2][NB];
 #pragma unroll
-      for (int kk = 0; kk < E::BK; kk += E::KSTEP) {
-        typename E::frag a[MB], b[NB];
+      for (int i = 0; i < MB; ++i) a[0][i] = read_frag<E, SA::LD>(sA, wm + 32 * i, 0, lane);
 #pragma unroll
-        for (int i = 0; i < MB; ++i) a[i] = read_frag<E, SA::LD, AK>(sA, wm + 32 * i, kk, lane);
+      for (int j = 0; j < NB; ++j) b[0][j] = read_frag<E, SB::LD>(sB, wn + 32 * j, 0, lane);
 #pragma unroll
-        for (int j = 0; j < NB; ++j) b[j] = read_frag<E, SB::LD, BKM>(sB, wn + 32 * j, kk, lane);
+      for (int q = 0; q < NKK; ++q) {
+        const int cur = q & 1;
+        if (q + 1 < NKK) {
+#pragma unroll
+          for (int i = 0; i < MB; ++i)
+            a[cur ^ 1][i] = read_frag<E, SA::LD>(sA, wm + 32 * i, (q + 1) * E::KSTEP, lane);
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            b[cur ^ 1][j] = read_frag<E, SB::LD>(sB, wn + 32 * j, (q + 1) * E::KSTEP, lane);
+        }
 #pragma unroll
         for (int i = 0; i < MB; ++i)
 #pragma unroll
-          for (int j = 0; j < NB; ++j) acc[i][j] = E::mma(a[i], b[j], acc[i][j]);
+          for (int j = 0; j < NB; ++j) acc[i][j] = E::mma(a[cur][i], b[cur][j], acc[i][j]);
       }
-      __syncthreads();
       if (more) {
-        la.store(sA, tid);
-        lb.store(sB, tid);
+        S* nA = smem + ((kt + 1) & 1) * BUF_ELEMS;
+        la.store(nA, tid);
+        lb.store(nA + SA::LDS_ELEMS, tid);
       }
       __syncthreads();
     }
   }
 };
+
+// ---------------------------------------------------------------------------
+// Workgroup -> tile mapping.  Workgroups are dispatched to the 8 XCDs round
+// robin (workgroup i on XCD i % 8) and each XCD has its own L2, so consecutive
+// logical tile ids are handed to the workgroups of one XCD: the tiles an XCD
+// runs at the same time then share operand panels in its L2.
+__device__ __forceinline__ int xcd_logical(int bid, int n) {
+  constexpr int X = 8;
+  const int q = n / X, r = n % X;
+  const int xcd = bid % X, local = bid / X;
+  return xcd < r ? xcd * (q + 1) + local : r * (q + 1) + (xcd - r) * q + local;
+}
+
+// Logical id -> (mt, nt) in column-major groups of GM tile rows, so that a run
+// of consecutive ids covers a GM x (run/GM) block of output tiles.
+__device__ __forceinline__ void grouped_tile(int logical, int n_m, int n_n, int GM, int& mt,
+                                             int& nt) {
+  const int per_group = GM * n_n;
+  const int group = logical / per_group;
+  const int first = group * GM;
+  const int gm = min(n_m - first, GM);
+  const int in = logical - group * per_group;
+  mt = first + in % gm;
+  nt = in / gm;
+}
 
 // ---------------------------------------------------------------------------
 // Online-softmax state merge in the base-2 domain (m is a running maximum of
@@ -217,16 +235,18 @@ __global__ void fill_zero_kernel(float* p, int64_t n) {
 // vocabulary tiles in visiting order; it folds every logits tile into a
 // per-lane online-softmax state, gathers the target logit from the one tile
 // whose rows contain it, and writes its partial (m, s) per token.
-template <class E, int BM, int BN>
-__global__ void __launch_bounds__(kThreads) fwd_kernel(FwdArgs a) {
-  using G = Gemm<E, BM, BN, true, true>;
+template <class E, class G>
+__global__ void __launch_bounds__(G::NT) fwd_kernel(FwdArgs a) {
   using S = typename E::storage;
+  constexpr int BM = G::BM, BN = G::BN, MB = G::MB, NB = G::NB;
   __shared__ __attribute__((aligned(16))) S smem[G::LDS_ELEMS];
-  constexpr int MB = G::MB, NB = G::NB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = (wave >> 1) * G::WM, wn = (wave & 1) * G::WN;
-  const int tb = blockIdx.x % a.n_tok_blocks;
-  const int split = blockIdx.x / a.n_tok_blocks;
+  const int wm = G::wave_m(wave), wn = G::wave_n(wave);
+  // split fastest: the workgroups an XCD runs together share token blocks (H panels)
+  // across splits and vocabulary tiles (W panels) across token blocks.
+  const int logical = xcd_logical(blockIdx.x, gridDim.x);
+  const int tb = logical / a.n_splits;
+  const int split = logical % a.n_splits;
   const int n0 = tb * BN;
   const int t_begin = (int)((int64_t)split * a.n_tiles / a.n_splits);
   const int t_end = (int)((int64_t)(split + 1) * a.n_tiles / a.n_splits);
@@ -301,7 +321,7 @@ __global__ void __launch_bounds__(kThreads) fwd_kernel(FwdArgs a) {
     }
   }
 
-  // Merge the two lane halves that share a token column, then the two wave rows.
+  // Merge the two lane halves that share a token column, then the wave rows.
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const float mo = __shfl_xor(m_run[j], 32);
@@ -309,20 +329,22 @@ __global__ void __launch_bounds__(kThreads) fwd_kernel(FwdArgs a) {
     merge_state(m_run[j], s_run[j], mo, so);
   }
   __syncthreads();  // smem is free after the last tile
-  float* red = (float*)smem;  // [2][BN]
-  if ((wave >> 1) == 1 && lane < 32) {
+  float* red = (float*)smem;  // [WGM][2][BN]
+  const int wr = wave / G::WGN;
+  if (lane < 32) {
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
-      red[wn + 32 * j + lane] = m_run[j];
-      red[BN + wn + 32 * j + lane] = s_run[j];
+      red[(wr * 2) * BN + wn + 32 * j + lane] = m_run[j];
+      red[(wr * 2 + 1) * BN + wn + 32 * j + lane] = s_run[j];
     }
   }
   __syncthreads();
-  if ((wave >> 1) == 0 && lane < 32) {
+  if (wr == 0 && lane < 32) {
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       const int c = wn + 32 * j + lane;
-      merge_state(m_run[j], s_run[j], red[c], red[BN + c]);
+      for (int w2 = 1; w2 < G::WGM; ++w2)
+        merge_state(m_run[j], s_run[j], red[(w2 * 2) * BN + c], red[(w2 * 2 + 1) * BN + c]);
       const int64_t n = n0 + c;
       if (n < a.T) {
         a.m_part[(int64_t)split * a.T + n] = m_run[j];
@@ -356,17 +378,20 @@ __global__ void __launch_bounds__(256) comb_kernel(CombArgs a) {
 }
 
 // Backward residual: recompute a logits tile of the (vocabulary chunk, token
-// chunk) strip and store G = g (2^(y log2e - lse log2e) - onehot) into the strip.
-template <class E, int BM, int BN>
-__global__ void __launch_bounds__(kThreads) grad_kernel(GradArgs a) {
-  using G = Gemm<E, BM, BN, true, true>;
+// chunk) strip and store G = g (2^(y log2e - lse log2e) - onehot) into the strip
+// in both layouts: G[v][t] (token columns contiguous, for dW) and G^T[t][v]
+// (vocabulary columns contiguous, for dH).  Rows and columns of the tile that
+// fall outside the chunk are written as zeros so that both contractions can
+// read whole 16-byte chunks past a ragged edge.
+template <class E, class G>
+__global__ void __launch_bounds__(G::NT) grad_kernel(GradArgs a) {
   using S = typename E::storage;
+  constexpr int BM = G::BM, BN = G::BN, MB = G::MB, NB = G::NB;
   __shared__ __attribute__((aligned(16))) S smem[G::LDS_ELEMS];
-  constexpr int MB = G::MB, NB = G::NB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = (wave >> 1) * G::WM, wn = (wave & 1) * G::WN;
-  const int vt = blockIdx.x % a.n_vt;
-  const int tb = blockIdx.x / a.n_vt;
+  const int wm = G::wave_m(wave), wn = G::wave_n(wave);
+  int vt, tb;
+  grouped_tile(xcd_logical(blockIdx.x, gridDim.x), a.n_vt, gridDim.x / a.n_vt, 4, vt, tb);
   const int m0 = vt * BM, n0 = tb * BN;
 
   f32x16_t acc[MB][NB];
@@ -376,37 +401,52 @@ __global__ void __launch_bounds__(kThreads) grad_kernel(GradArgs a) {
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
   G::run(acc, (const S*)a.W, a.d, m0, a.M, (const S*)a.H + a.t0 * a.d, a.d, n0, a.N, a.d, smem);
 
-  S* Gs = (S*)a.strip;
+  // Strip offsets fit in 32 bits (the strip budget is capped below 2^31 elements).
+  S* __restrict__ Gs = (S*)a.strip;
+  S* __restrict__ Gt = (S*)a.strip_t;
+  const uint32_t ldg = (uint32_t)a.ldg, ldgt = (uint32_t)a.ldgt;
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int nl = n0 + wn + 32 * j + (lane & 31);  // token column within the chunk
     float lse2 = 0.f, g = 0.f;
-    int64_t tg = a.ignore_index;
+    int rel = -1;  // target row within the chunk, or -1
     bool live = false, bad = false;
     if (nl < a.N) {
       const int64_t t = a.t0 + nl;
-      tg = a.targets[t];
+      const int64_t tg = a.targets[t];
       if (tg != a.ignore_index) {
         bad = tg < 0 || tg >= a.V;
         live = true;
         lse2 = a.lse[t] * kLog2e;
         g = a.grad[t];
+        const int64_t r64 = tg - a.gid0;
+        rel = (r64 >= 0 && r64 < a.M) ? (int)r64 : -1;
       }
     }
-    const int64_t rel = tg - a.gid0;  // target row within the chunk (if any)
+    if (bad) g = __builtin_nanf("");
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int ml = m0 + wm + 32 * i + acc_row(r, lane);
-        if (ml < a.M) {
-          float v = 0.f;
-          if (live) {
-            const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r], kLog2e, -lse2));
-            v = g * (p - (rel == (int64_t)ml ? 1.f : 0.f));
-            if (bad) v = __builtin_nanf("");
-          }
-          Gs[(int64_t)ml * a.ldg + nl] = E::from_f32(v);
+      for (int r4 = 0; r4 < 16; r4 += 4) {
+        // registers r4..r4+3 hold 4 consecutive vocabulary rows of token column nl
+        const int ml0 = m0 + wm + 32 * i + acc_row(r4, lane);
+        S v4[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int ml = ml0 + q;
+          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r4 + q], kLog2e, -lse2));
+          const float v = (live && ml < a.M) ? g * (p - (rel == ml ? 1.f : 0.f)) : 0.f;
+          v4[q] = E::from_f32(v);
+          Gs[(uint32_t)ml * ldg + (uint32_t)nl] = v4[q];
+        }
+        const uint32_t ot = (uint32_t)nl * ldgt + (uint32_t)ml0;
+        if constexpr (sizeof(S) == 2) {
+          uint2 packed;
+          packed.x = (uint32_t)v4[0] | ((uint32_t)v4[1] << 16);
+          packed.y = (uint32_t)v4[2] | ((uint32_t)v4[3] << 16);
+          *(uint2*)(Gt + ot) = packed;
+        } else {
+          *(float4*)(Gt + ot) = make_float4(v4[0], v4[1], v4[2], v4[3]);
         }
       }
   }
@@ -422,26 +462,24 @@ __global__ void count_bad_kernel(const int64_t* targets, int64_t T, int64_t V, i
   }
 }
 
-// Plain tile GEMM with a float32 output: C = (beta ? C : 0) + A * B.
-template <class E, int BM, int BN, bool AK, bool BKM>
-__global__ void __launch_bounds__(kThreads) gemm_kernel(GemmArgs a) {
-  using G = Gemm<E, BM, BN, AK, BKM>;
+// Two independent tile GEMMs with float32 outputs, C = (beta ? C : 0) + A B^T,
+// in one launch: the first tiles0 workgroups take problem 0, the rest problem
+// 1.  One launch for the dH and dW contractions of a strip halves the partly
+// filled last round of workgroups.
+template <class E, class G>
+__device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int nt,
+                                          typename E::storage* smem) {
   using S = typename E::storage;
-  __shared__ __attribute__((aligned(16))) S smem[G::LDS_ELEMS];
-  constexpr int MB = G::MB, NB = G::NB;
+  constexpr int BM = G::BM, BN = G::BN, MB = G::MB, NB = G::NB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = (wave >> 1) * G::WM, wn = (wave & 1) * G::WN;
-  const int nt = blockIdx.x % a.n_nt;
-  const int mt = blockIdx.x / a.n_nt;
+  const int wm = G::wave_m(wave), wn = G::wave_n(wave);
   const int m0 = mt * BM, n0 = nt * BN;
-
   f32x16_t acc[MB][NB];
 #pragma unroll
   for (int i = 0; i < MB; ++i)
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
   G::run(acc, (const S*)a.A, a.lda, m0, a.M, (const S*)a.B, a.ldb, n0, a.N, a.K, smem);
-
 #pragma unroll
   for (int i = 0; i < MB; ++i)
 #pragma unroll
@@ -457,58 +495,125 @@ __global__ void __launch_bounds__(kThreads) gemm_kernel(GemmArgs a) {
     }
 }
 
-// ---------------------------------------------------------------------------
-// Launchers (host side).  Tile shapes are fixed per element type.
-template <class E> struct Tiles;
-template <> struct Tiles<Bf16> {
-  static constexpr int FWD_BM = 128, FWD_BN = 128;
-  static constexpr int GRAD_BM = 128, GRAD_BN = 128;
-  static constexpr int MM_BM = 128, MM_BN = 128;
+// Per-XCD split of a two-problem grid: XCD x runs cnt0[x] tiles of problem 0
+// (numbered from first0[x]) and then its share of problem 1 (from first1[x]), so
+// that every XCD gets an even share of both problems and consecutive tiles of
+// one problem stay on one XCD's L2.
+struct PairSplit {
+  int32_t cnt0[8], first0[8], first1[8];
 };
-template <> struct Tiles<F32> {
-  static constexpr int FWD_BM = 64, FWD_BN = 64;
-  static constexpr int GRAD_BM = 64, GRAD_BN = 64;
-  static constexpr int MM_BM = 64, MM_BN = 64;
+
+template <class E, class G>
+__global__ void __launch_bounds__(G::NT) gemm_pair_kernel(GemmArgs a0, GemmArgs a1, PairSplit sp) {
+  using S = typename E::storage;
+  __shared__ __attribute__((aligned(16))) S smem[G::LDS_ELEMS];
+  const int xcd = blockIdx.x % 8, local = blockIdx.x / 8;
+  int mt, nt;
+  if (local < sp.cnt0[xcd]) {
+    const int n_n = (a0.N + G::BN - 1) / G::BN, n_m = (a0.M + G::BM - 1) / G::BM;
+    grouped_tile(sp.first0[xcd] + local, n_m, n_n, 4, mt, nt);
+    gemm_tile<E, G>(a0, mt, nt, smem);
+  } else {
+    const int n_n = (a1.N + G::BN - 1) / G::BN, n_m = (a1.M + G::BM - 1) / G::BM;
+    grouped_tile(sp.first1[xcd] + local - sp.cnt0[xcd], n_m, n_n, 4, mt, nt);
+    gemm_tile<E, G>(a1, mt, nt, smem);
+  }
+}
+
+// out[c][r] = in[r][c] through a 64 x 64 LDS tile; rows R..R_pad-1 of the
+// output's columns are zero-filled.
+template <class S>
+__global__ void __launch_bounds__(256) transpose_kernel(TransposeArgs a) {
+  __shared__ S tile[64][65];
+  const S* in = (const S*)a.in;
+  S* out = (S*)a.out;
+  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+  for (int i = ty; i < 64; i += 4) {
+    const int r = r0 + i, c = c0 + tx;
+    tile[i][tx] = (r < a.R && c < a.C) ? in[(int64_t)r * a.ld_in + c] : (S)0;
+  }
+  __syncthreads();
+  for (int i = ty; i < 64; i += 4) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < a.C && r < a.R_pad) out[(int64_t)c * a.ld_out + r] = tile[tx][i];
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Tile configurations.  bf16: 512 threads (two wavefronts per SIMD, so one
+// wave's LDS waits overlap the other's MFMAs).
+//   logits (forward / recompute): 256 vocabulary rows x 256 tokens, waves 2 x 4
+//   dH / dW: 256 x 192 (waves 4 x 2) when d is a multiple of 192 but not of 256
+//            (d = 2880 = 15 x 192), else 256 x 256 (waves 2 x 4)
+// f32: 64 x 64 tiles, 256 threads (waves 2 x 2).
+template <class E> struct Cfg;
+template <> struct Cfg<Bf16> {
+  using Logits = Gemm<Bf16, 256, 256, 2, 4>;
+  using MmA = Gemm<Bf16, 256, 256, 2, 4>;
+  using MmB = Gemm<Bf16, 256, 192, 4, 2>;
+};
+template <> struct Cfg<F32> {
+  using Logits = Gemm<F32, 64, 64, 2, 2>;
+  using MmA = Gemm<F32, 64, 64, 2, 2>;
+  using MmB = Gemm<F32, 64, 64, 2, 2>;
 };
 
 static inline bool launched_ok() { return hipGetLastError() == hipSuccess; }
 
 template <class E>
 static bool launch_fwd(const FwdArgs& a, hipStream_t s) {
-  constexpr int BM = Tiles<E>::FWD_BM, BN = Tiles<E>::FWD_BN;
+  using G = typename Cfg<E>::Logits;
   const unsigned grid = (unsigned)(a.n_tok_blocks * a.n_splits);
-  hipLaunchKernelGGL((fwd_kernel<E, BM, BN>), dim3(grid), dim3(kThreads), 0, s, a);
+  hipLaunchKernelGGL((fwd_kernel<E, G>), dim3(grid), dim3(G::NT), 0, s, a);
   return launched_ok();
 }
 template <class E>
 static bool launch_grad(const GradArgs& a, hipStream_t s) {
-  constexpr int BM = Tiles<E>::GRAD_BM, BN = Tiles<E>::GRAD_BN;
-  const unsigned grid = (unsigned)(a.n_vt * ((a.N + BN - 1) / BN));
-  hipLaunchKernelGGL((grad_kernel<E, BM, BN>), dim3(grid), dim3(kThreads), 0, s, a);
+  using G = typename Cfg<E>::Logits;
+  const unsigned grid = (unsigned)(a.n_vt * ((a.N + G::BN - 1) / G::BN));
+  hipLaunchKernelGGL((grad_kernel<E, G>), dim3(grid), dim3(G::NT), 0, s, a);
   return launched_ok();
 }
-template <class E, bool AK, bool BKM>
-static bool launch_gemm(GemmArgs a, hipStream_t s) {
-  constexpr int BM = Tiles<E>::MM_BM, BN = Tiles<E>::MM_BN;
-  a.n_nt = (a.N + BN - 1) / BN;
-  const unsigned grid = (unsigned)(a.n_nt * ((a.M + BM - 1) / BM));
-  hipLaunchKernelGGL((gemm_kernel<E, BM, BN, AK, BKM>), dim3(grid), dim3(kThreads), 0, s, a);
+template <class E, class G>
+static bool launch_pair_tiles(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
+  const int t0 = a0.M > 0 ? ((a0.M + G::BM - 1) / G::BM) * ((a0.N + G::BN - 1) / G::BN) : 0;
+  const int t1 = a1.M > 0 ? ((a1.M + G::BM - 1) / G::BM) * ((a1.N + G::BN - 1) / G::BN) : 0;
+  const int n = t0 + t1;
+  if (n == 0) return true;
+  // workgroup b runs on XCD b % 8: XCD x receives n/8 (+1 for x < n%8) of them
+  PairSplit sp;
+  int f0 = 0, f1 = 0;
+  for (int x = 0; x < 8; ++x) {
+    const int cnt = n / 8 + (x < n % 8 ? 1 : 0);
+    const int c0 = t0 / 8 + (x < t0 % 8 ? 1 : 0);  // <= cnt (see the argument below)
+    sp.cnt0[x] = c0;
+    sp.first0[x] = f0;
+    sp.first1[x] = f1;
+    f0 += c0;
+    f1 += cnt - c0;
+  }
+  // c0 <= cnt: if n/8 > t0/8 this is immediate; if they are equal then n%8 >= t0%8.
+  hipLaunchKernelGGL((gemm_pair_kernel<E, G>), dim3((unsigned)n), dim3(G::NT), 0, s, a0, a1, sp);
   return launched_ok();
 }
-
-}  // namespace vpce
+template <class E>
+static bool launch_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
+  // both problems share N (= d)
+  if (a0.N % 256 != 0 && a0.N % 192 == 0)
+    return launch_pair_tiles<E, typename Cfg<E>::MmB>(a0, a1, s);
+  return launch_pair_tiles<E, typename Cfg<E>::MmA>(a0, a1, s);
+}
 
 // ---- entry points used by the host API (vpce_api.cpp) ----
-namespace vpce {
-
 TileShape tile_shape(int dtype) {
   TileShape t;
   if (dtype == 1) {
-    t.fwd_bm = Tiles<Bf16>::FWD_BM; t.fwd_bn = Tiles<Bf16>::FWD_BN;
-    t.grad_bm = Tiles<Bf16>::GRAD_BM; t.grad_bn = Tiles<Bf16>::GRAD_BN;
+    t.fwd_bm = t.grad_bm = Cfg<Bf16>::Logits::BM;
+    t.fwd_bn = t.grad_bn = Cfg<Bf16>::Logits::BN;
   } else {
-    t.fwd_bm = Tiles<F32>::FWD_BM; t.fwd_bn = Tiles<F32>::FWD_BN;
-    t.grad_bm = Tiles<F32>::GRAD_BM; t.grad_bn = Tiles<F32>::GRAD_BN;
+    t.fwd_bm = t.grad_bm = Cfg<F32>::Logits::BM;
+    t.fwd_bn = t.grad_bn = Cfg<F32>::Logits::BN;
   }
   return t;
 }
@@ -541,13 +646,17 @@ bool run_count_bad(const int64_t* targets, int64_t T, int64_t V, int64_t ignore_
                      T, V, ignore_index, counter);
   return launched_ok();
 }
-bool run_dH(int dtype, const GemmArgs& a, hipStream_t s) {
-  // C[t][n] = sum_v G[v][t] W[v][n]: A (strip) and B (W) both MN-major.
-  return dtype == 1 ? launch_gemm<Bf16, false, false>(a, s) : launch_gemm<F32, false, false>(a, s);
+bool run_gemm_pair(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
+  return dtype == 1 ? launch_pair<Bf16>(a0, a1, s) : launch_pair<F32>(a0, a1, s);
 }
-bool run_dW(int dtype, const GemmArgs& a, hipStream_t s) {
-  // C[v][n] = sum_t G[v][t] H[t][n]: A (strip) K-major, B (H) MN-major.
-  return dtype == 1 ? launch_gemm<Bf16, true, false>(a, s) : launch_gemm<F32, true, false>(a, s);
+bool run_transpose(int dtype, const TransposeArgs& a, hipStream_t s) {
+  if (a.C <= 0 || a.R_pad <= 0) return true;
+  const dim3 grid((unsigned)((a.R_pad + 63) / 64), (unsigned)((a.C + 63) / 64));
+  if (dtype == 1)
+    hipLaunchKernelGGL(transpose_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(transpose_kernel<float>, grid, dim3(256), 0, s, a);
+  return launched_ok();
 }
 
 }  // namespace vpce
