@@ -303,7 +303,7 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
         tr.ld_out = plan.Vc;
         tr.R = (int32_t)M;
         tr.C = (int32_t)d;
-        tr.R_pad = (int32_t)round_up(M, 8);
+        tr.R_pad = (int32_t)round_up(M, 32);
         if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
       }
       for (int64_t t0 = 0; t0 < T; t0 += tc) {
@@ -337,7 +337,7 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
         h.ldc = d;
         h.M = (int32_t)N;
         h.N = (int32_t)d;
-        h.K = (int32_t)M;
+        h.K = (int32_t)round_up(M, ts.kalign);  // G^T and W^T are zero past M
         h.beta = first_vchunk ? 0 : 1;
 
         vpce::GemmArgs w;  // dW_chunk (+)= G H[t0 : t0+N] = G . (H^T)^T
@@ -349,7 +349,7 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
         w.ldc = d;
         w.M = (int32_t)M;
         w.N = (int32_t)d;
-        w.K = (int32_t)N;
+        w.K = (int32_t)round_up(N, ts.kalign);  // G is zero past N
         w.beta = (t0 > 0 || accumulate) ? 1 : 0;
         if (!vpce::run_gemm_pair(prob->dtype, h, w, s)) return VP_ERR_HIP;
       }

@@ -84,6 +84,7 @@ struct TransposeArgs {
 
 struct TileShape {
   int fwd_bm, fwd_bn, grad_bm, grad_bn;
+  int kalign;  // the dH / dW contractions are launched with K rounded up to this
 };
 
 TileShape tile_shape(int dtype);

@@ -188,6 +188,126 @@ struct Gemm {
 };
 
 // ---------------------------------------------------------------------------
+// bf16 tile GEMM fed by direct global -> LDS loads (global_load_lds_dwordx4,
+// 16 bytes per lane straight into LDS, no staging registers) through a ring of
+// STAGES k-slices of BK = 32, so that STAGES-1 slices are in flight while one
+// is multiplied.  Requires K to be a multiple of 32 and both operands to hold
+// finite values up to that K (the backward's buffers are zero-padded).
+//
+// LDS slice layout: the A rows then the B rows, 64 bytes (four 16-byte chunks)
+// per row, chunk c of row r stored in slot c ^ ((r >> 2) & 3): the 16 lanes of
+// one LDS read phase (16 consecutive rows, same chunk) then hit 16 distinct
+// 4-bank groups, and each load instruction writes 1 KiB contiguously (16 rows).
+//
+// The loads are issued from inline assembly so that the compiler, which cannot
+// tell which ring slot an LDS read touches, does not drain every load in flight
+// before each read; completion is tracked by hand: before the barrier that
+// opens slice kt, a wave waits until only the loads of the STAGES-2 younger
+// slices are outstanding (loads return in issue order).  Slices past the end
+// are loaded anyway (a clamped, valid address) so the count stays constant.
+__device__ __forceinline__ void lds_dma16(const void* gsrc, uint32_t lds_byte_addr) {
+  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(gsrc), "{m0}"(lds_byte_addr) : "memory");
+}
+
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  // s_waitcnt simm16 on gfx9: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14
+  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+}
+
+template <int BM_, int BN_, int WGM_, int WGN_, int STAGES = 4>
+struct GemmDma {
+  using S = uint16_t;
+  static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
+  static constexpr int NT = 64 * WGM * WGN, NWAVES = WGM * WGN;
+  static constexpr int WM = BM / WGM, WN = BN / WGN, MB = WM / 32, NB = WN / 32;
+  static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be whole 32x32 blocks");
+  static constexpr int BK = 32;
+  static constexpr int ROWS = BM + BN;            // rows of one slice (A then B)
+  static constexpr int SLICE_BYTES = ROWS * 64;
+  static constexpr int GROUPS = ROWS / 16;        // 1 KiB load instructions per slice
+  static_assert(ROWS % 16 == 0, "slice rows");
+  static constexpr int G_LO = GROUPS / NWAVES, G_REM = GROUPS % NWAVES;  // waves < G_REM do one more
+  static constexpr int LDS_ELEMS = STAGES * SLICE_BYTES / 2;
+
+  __device__ __forceinline__ static int wave_m(int wave) { return (wave / WGN) * WM; }
+  __device__ __forceinline__ static int wave_n(int wave) { return (wave % WGN) * WN; }
+
+  // Issue this wave's loads of slice kt into ring slot (kt % STAGES).
+  __device__ __forceinline__ static void issue(const S* __restrict__ A, int64_t lda, int m0, int M,
+                                               const S* __restrict__ B, int64_t ldb, int n0, int N,
+                                               int kt, int nk, uint32_t lds0, int wave, int lane) {
+    const int kc = min(kt, nk - 1) * BK;  // past the end: reload the last slice (never read)
+    const uint32_t slot_base = lds0 + (uint32_t)((kt % STAGES) * SLICE_BYTES);
+    const int row_in = lane >> 2;         // 16 rows per instruction, 4 lanes per row
+#pragma unroll
+    for (int q = 0; q < G_LO + 1; ++q) {
+      if (q == G_LO && wave >= G_REM) break;
+      const int g = wave + q * NWAVES;
+      const int r = g * 16 + row_in;    // row within the slice
+      const int chunk = (lane & 3) ^ ((r >> 2) & 3);
+      const S* src;
+      if (r < BM) {
+        src = A + (int64_t)min(m0 + r, M - 1) * lda + kc + 8 * chunk;
+      } else {
+        src = B + (int64_t)min(n0 + r - BM, N - 1) * ldb + kc + 8 * chunk;
+      }
+      lds_dma16(src, slot_base + (uint32_t)(g * 1024));
+    }
+  }
+
+  __device__ __forceinline__ static bf16x8_t frag(const S* slot, int row, int chunk) {
+    return *(const bf16x8_t*)(slot + row * 32 + ((chunk ^ ((row >> 2) & 3)) << 3));
+  }
+
+  __device__ __forceinline__ static void run(f32x16_t (&acc)[MB][NB], const S* __restrict__ A,
+                                             int64_t lda, int m0, int M, const S* __restrict__ B,
+                                             int64_t ldb, int n0, int N, int K, S* smem) {
+    // The wave index is made scalar so that the per-wave load counts below are
+    // taken on scalar branches: a vmcnt wait on a skipped path must not execute.
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int wm = wave_m(wave), wn = wave_n(wave);
+    const int nk = K / BK;
+    if (nk <= 0) return;
+    const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) S*)smem;
+#pragma unroll
+    for (int kt = 0; kt < STAGES - 1; ++kt) issue(A, lda, m0, M, B, ldb, n0, N, kt, nk, lds0, wave, lane);
+    for (int kt = 0; kt < nk; ++kt) {
+      // this wave's loads of slice kt are done once only the STAGES-2 younger slices remain
+      if (wave < G_REM)
+        wait_vmcnt<(STAGES - 2) * (G_LO + 1)>();
+      else
+        wait_vmcnt<(STAGES - 2) * G_LO>();
+      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS reads of the last slice are done
+      __builtin_amdgcn_s_barrier();
+      // slot (kt-1) % STAGES is free now: refill it with slice kt + STAGES - 1
+      issue(A, lda, m0, M, B, ldb, n0, N, kt + STAGES - 1, nk, lds0, wave, lane);
+      const S* slot = smem + (kt % STAGES) * (SLICE_BYTES / 2);
+#pragma unroll
+      for (int kk = 0; kk < BK / 16; ++kk) {
+        bf16x8_t a[MB], b[NB];
+        const int chunk = 2 * kk + (lane >> 5);
+#pragma unroll
+        for (int i = 0; i < MB; ++i) a[i] = frag(slot, wm + 32 * i + (lane & 31), chunk);
+#pragma unroll
+        for (int j = 0; j < NB; ++j) b[j] = frag(slot, BM + wn + 32 * j + (lane & 31), chunk);
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+          for (int j = 0; j < NB; ++j)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      }
+    }
+    // drain: no load may still be writing LDS when the caller reuses it
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_waitcnt(0xC07F);
+    __builtin_amdgcn_s_barrier();
+  }
+};
+
+// ---------------------------------------------------------------------------
 // Workgroup -> tile mapping.  Workgroups are dispatched to the 8 XCDs round
 // robin (workgroup i on XCD i % 8) and each XCD has its own L2, so consecutive
 // logical tile ids are handed to the workgroups of one XCD: the tiles an XCD
@@ -542,38 +662,51 @@ __global__ void __launch_bounds__(256) transpose_kernel(TransposeArgs a) {
 
 // ---------------------------------------------------------------------------
 // Tile configurations.  bf16: 512 threads (two wavefronts per SIMD, so one
-// wave's LDS waits overlap the other's MFMAs).
+// wave's waits overlap the other's MFMAs), direct-to-LDS 4-slice ring.
 //   logits (forward / recompute): 256 vocabulary rows x 256 tokens, waves 2 x 4
+//     (register-staged double buffer when d is not a multiple of 32)
 //   dH / dW: 256 x 192 (waves 4 x 2) when d is a multiple of 192 but not of 256
 //            (d = 2880 = 15 x 192), else 256 x 256 (waves 2 x 4)
-// f32: 64 x 64 tiles, 256 threads (waves 2 x 2).
+// f32: 64 x 64 tiles, 256 threads (waves 2 x 2), register-staged.
 template <class E> struct Cfg;
 template <> struct Cfg<Bf16> {
-  using Logits = Gemm<Bf16, 256, 256, 2, 4>;
-  using MmA = Gemm<Bf16, 256, 256, 2, 4>;
-  using MmB = Gemm<Bf16, 256, 192, 4, 2>;
+  using Logits = GemmDma<256, 256, 2, 4>;
+  using LogitsReg = Gemm<Bf16, 256, 256, 2, 4>;
+  using MmA = GemmDma<256, 256, 2, 4>;
+  using MmB = GemmDma<256, 192, 4, 2>;
+  static constexpr int KALIGN = 32;  // K granularity the dH / dW launches need
 };
 template <> struct Cfg<F32> {
   using Logits = Gemm<F32, 64, 64, 2, 2>;
+  using LogitsReg = Logits;
   using MmA = Gemm<F32, 64, 64, 2, 2>;
   using MmB = Gemm<F32, 64, 64, 2, 2>;
+  static constexpr int KALIGN = 1;
 };
 
 static inline bool launched_ok() { return hipGetLastError() == hipSuccess; }
 
-template <class E>
-static bool launch_fwd(const FwdArgs& a, hipStream_t s) {
-  using G = typename Cfg<E>::Logits;
+template <class E, class G>
+static bool launch_fwd_g(const FwdArgs& a, hipStream_t s) {
   const unsigned grid = (unsigned)(a.n_tok_blocks * a.n_splits);
   hipLaunchKernelGGL((fwd_kernel<E, G>), dim3(grid), dim3(G::NT), 0, s, a);
   return launched_ok();
 }
 template <class E>
-static bool launch_grad(const GradArgs& a, hipStream_t s) {
-  using G = typename Cfg<E>::Logits;
+static bool launch_fwd(const FwdArgs& a, hipStream_t s) {
+  if (a.d % 32 == 0) return launch_fwd_g<E, typename Cfg<E>::Logits>(a, s);
+  return launch_fwd_g<E, typename Cfg<E>::LogitsReg>(a, s);
+}
+template <class E, class G>
+static bool launch_grad_g(const GradArgs& a, hipStream_t s) {
   const unsigned grid = (unsigned)(a.n_vt * ((a.N + G::BN - 1) / G::BN));
   hipLaunchKernelGGL((grad_kernel<E, G>), dim3(grid), dim3(G::NT), 0, s, a);
   return launched_ok();
+}
+template <class E>
+static bool launch_grad(const GradArgs& a, hipStream_t s) {
+  if (a.d % 32 == 0) return launch_grad_g<E, typename Cfg<E>::Logits>(a, s);
+  return launch_grad_g<E, typename Cfg<E>::LogitsReg>(a, s);
 }
 template <class E, class G>
 static bool launch_pair_tiles(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
@@ -607,13 +740,18 @@ static bool launch_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
 
 // ---- entry points used by the host API (vpce_api.cpp) ----
 TileShape tile_shape(int dtype) {
+  static_assert(Cfg<Bf16>::Logits::BM == Cfg<Bf16>::LogitsReg::BM &&
+                    Cfg<Bf16>::Logits::BN == Cfg<Bf16>::LogitsReg::BN,
+                "both logits mainloops must share the tile shape");
   TileShape t;
   if (dtype == 1) {
     t.fwd_bm = t.grad_bm = Cfg<Bf16>::Logits::BM;
     t.fwd_bn = t.grad_bn = Cfg<Bf16>::Logits::BN;
+    t.kalign = Cfg<Bf16>::KALIGN;
   } else {
     t.fwd_bm = t.grad_bm = Cfg<F32>::Logits::BM;
     t.fwd_bn = t.grad_bn = Cfg<F32>::Logits::BN;
+    t.kalign = Cfg<F32>::KALIGN;
   }
   return t;
 }
