@@ -82,7 +82,7 @@ typedef struct {
   int64_t ignore_index;       /* target value that marks a token without loss (e.g. -100) */
   uint32_t flags;             /* VP_ACCUMULATE_DW */
   int64_t strip_elems;        /* backward residual-strip budget in elements per layout,
-                                 0..2^30; 0 = default (64 Mi) */
+                                 0..2^30; 0 = default (100 Mi) */
 } vp_problem;
 
 /* Workspace sizes in bytes for vp_ce_forward (*fwd_bytes) and vp_ce_backward

@@ -8,6 +8,7 @@
 
 #include <algorithm>
 #include <cmath>
+#include <vector>
 
 #include "vpce_internal.h"
 
@@ -66,15 +67,17 @@ size_t fwd_ws_bytes(const vp_problem* p) {
 }
 
 // Backward plan.  The softmax residual of a strip of Tc tokens by Vc
-// vocabulary rows is staged in both layouts (G [Vc][Tc] and G^T [Tc][Vc]);
-// Tc*Vc <= budget, as square as the token count allows (the float32
-// read-modify-write traffic of dH across vocabulary chunks plus that of dW
-// across token chunks is proportional to 1/Vc + 1/Tc).  The workspace also
-// holds H^T [d][T_pad] (written once per call) and W^T [d][Vc] of the current
-// vocabulary chunk.  Nothing here depends on V.
+// vocabulary rows is staged in both layouts (G [Vc][Tc] and G^T [Tc][Vc]),
+// twice: one launch writes the residual of strip c+1 while it contracts strip
+// c into dH and dW.  Tc*Vc <= budget; tokens in balanced chunks no larger than
+// the square root of the budget (the float32 read-modify-write traffic of dH
+// across vocabulary chunks plus that of dW across token chunks is proportional
+// to 1/Vc + 1/Tc).  The workspace also holds H^T [d][T_pad] (written once per
+// call) and W^T [d][Vc] of the current vocabulary chunk.  Nothing here depends
+// on V.
 struct StripPlan {
   int64_t Tc, Vc, T_pad;
-  size_t off_g, off_gt, off_ht, off_wt, total;
+  size_t off_g[2], off_gt[2], off_ht, off_wt, total;
 };
 
 StripPlan strip_plan(const vp_problem* p) {
@@ -83,16 +86,19 @@ StripPlan strip_plan(const vp_problem* p) {
   const int64_t T = std::max<int64_t>(p->T, 1);
   const int64_t side = std::max<int64_t>(ts.grad_bn, round_down((int64_t)std::sqrt((double)budget), ts.grad_bn));
   StripPlan s;
-  // Tokens: ceil(T / side) balanced, tile-aligned chunks; vocabulary rows: the
-  // rest of the budget, tile-aligned.
   s.Tc = std::min<int64_t>(round_up(T, ts.grad_bn), round_up(ceil_div(T, ceil_div(T, side)), ts.grad_bn));
   s.Vc = std::max<int64_t>(ts.grad_bm, std::min<int64_t>(round_down(budget / s.Tc, ts.grad_bm),
                                                         32768));
-  s.T_pad = round_up(std::max<int64_t>(p->T, 1), 256);
+  s.T_pad = round_up(T, 256);
   const size_t eb = elem_bytes(p->dtype);
-  s.off_g = kHeaderBytes;
-  s.off_gt = s.off_g + align256((size_t)s.Vc * s.Tc * eb);
-  s.off_ht = s.off_gt + align256((size_t)s.Tc * s.Vc * eb);
+  const size_t strip = align256((size_t)s.Vc * s.Tc * eb);
+  size_t off = kHeaderBytes;
+  for (int b = 0; b < 2; ++b) {
+    s.off_g[b] = off;
+    s.off_gt[b] = off + strip;
+    off += 2 * strip;
+  }
+  s.off_ht = off;
   s.off_wt = s.off_ht + align256((size_t)p->d * s.T_pad * eb);
   s.total = s.off_wt + align256((size_t)p->d * s.Vc * eb);
   return s;
@@ -257,8 +263,6 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
   const vpce::TileShape ts = vpce::tile_shape(prob->dtype);
   const StripPlan plan = strip_plan(prob);
   char* wsb = (char*)ws;
-  void* strip = wsb + plan.off_g;
-  void* strip_t = wsb + plan.off_gt;
   void* Ht = wsb + plan.off_ht;
   void* Wt = wsb + plan.off_wt;
   const size_t eb = elem_bytes(prob->dtype);
@@ -275,86 +279,108 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
     if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
   }
 
+  // The strips in visiting order: shards in `order`, each cut into balanced,
+  // tile-aligned vocabulary chunks (never above Vc), each chunk meeting every
+  // token chunk.
+  struct Chunk {
+    int q;
+    int64_t v0, M, t0, N;
+    bool new_vchunk, first_vchunk;
+  };
+  std::vector<Chunk> chunks;
+  {
+    bool first = true;
+    for (int i = 0; i < prob->P; ++i) {
+      const int q = prob->order ? prob->order[i] : i;
+      const int64_t Vq = prob->shard_rows[q];
+      if (Vq == 0) continue;
+      const int64_t vc = std::min<int64_t>(
+          plan.Vc, round_up(ceil_div(Vq, ceil_div(Vq, plan.Vc)), ts.grad_bm));
+      for (int64_t v0 = 0; v0 < Vq; v0 += vc) {
+        for (int64_t t0 = 0; t0 < T; t0 += plan.Tc)
+          chunks.push_back({q, v0, std::min<int64_t>(vc, Vq - v0), t0,
+                            std::min<int64_t>(plan.Tc, T - t0), t0 == 0, first});
+        first = false;
+      }
+    }
+  }
   int64_t off[VP_MAX_SHARDS];
   int64_t acc = 0;
   for (int q = 0; q < prob->P; ++q) {
     off[q] = acc;
     acc += prob->shard_rows[q];
   }
-  // Balanced chunks: a shard of Vq rows is cut into ceil(Vq / Vc) chunks of equal
-  // tile-aligned size (never above the planned Vc), the tokens likewise.
-  const int64_t tc = plan.Tc;
-  bool first_vchunk = true;
-  for (int i = 0; i < prob->P; ++i) {
-    const int q = prob->order ? prob->order[i] : i;
-    const int64_t Vq = prob->shard_rows[q];
-    if (Vq == 0) continue;
-    const int64_t vc = std::min<int64_t>(
-        plan.Vc, round_up(ceil_div(Vq, ceil_div(Vq, plan.Vc)), ts.grad_bm));
-    for (int64_t v0 = 0; v0 < Vq; v0 += vc) {
-      const int64_t M = std::min<int64_t>(vc, Vq - v0);
-      const char* Wc = (const char*)W_shards[q] + (size_t)v0 * d * eb;
-      float* dWc = dW_shards[q] + v0 * d;
-      {  // W^T of this chunk, [d][Vc], zero beyond M
+  auto wchunk = [&](const Chunk& c) {
+    return (const char*)W_shards[c.q] + (size_t)c.v0 * d * eb;
+  };
+  // Launch k runs the residual of strip k (into buffer k % 2) and the dH / dW
+  // contractions of strip k-1 (from buffer (k-1) % 2).  Stream order gives every
+  // dependency: strip k-1 was written by launch k-1; buffer k % 2 was last read
+  // by launch k-1; dH rows and dW chunks are only updated by consecutive launches.
+  const int64_t n = (int64_t)chunks.size();
+  for (int64_t k = 0; k <= n; ++k) {
+    vpce::GradArgs g;
+    memset(&g, 0, sizeof(g));
+    if (k < n) {
+      const Chunk& c = chunks[k];
+      g.W = wchunk(c);
+      g.H = H;
+      g.targets = targets;
+      g.lse = lse;
+      g.grad = grad_loss;
+      g.strip = wsb + plan.off_g[k % 2];
+      g.strip_t = wsb + plan.off_gt[k % 2];
+      g.ldg = plan.Tc;
+      g.ldgt = plan.Vc;
+      g.t0 = c.t0;
+      g.gid0 = off[c.q] + c.v0;
+      g.V = V;
+      g.ignore_index = prob->ignore_index;
+      g.M = (int32_t)c.M;
+      g.N = (int32_t)c.N;
+      g.d = (int32_t)d;
+      g.n_vt = (int32_t)ceil_div(c.M, ts.grad_bm);
+    }
+    vpce::GemmArgs h, w;
+    memset(&h, 0, sizeof(h));
+    memset(&w, 0, sizeof(w));
+    if (k >= 1) {
+      const Chunk& c = chunks[k - 1];
+      if (c.new_vchunk) {  // W^T of this vocabulary chunk, [d][Vc], zero beyond M
         vpce::TransposeArgs tr;
-        tr.in = Wc;
+        tr.in = wchunk(c);
         tr.ld_in = d;
         tr.out = Wt;
         tr.ld_out = plan.Vc;
-        tr.R = (int32_t)M;
+        tr.R = (int32_t)c.M;
         tr.C = (int32_t)d;
-        tr.R_pad = (int32_t)round_up(M, 32);
+        tr.R_pad = (int32_t)round_up(c.M, 64);  // >= the K the dH launch reads
         if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
       }
-      for (int64_t t0 = 0; t0 < T; t0 += tc) {
-        const int64_t N = std::min<int64_t>(tc, T - t0);
-        vpce::GradArgs g;
-        g.W = Wc;
-        g.H = H;
-        g.targets = targets;
-        g.lse = lse;
-        g.grad = grad_loss;
-        g.strip = strip;
-        g.strip_t = strip_t;
-        g.ldg = plan.Tc;
-        g.ldgt = plan.Vc;
-        g.t0 = t0;
-        g.gid0 = off[q] + v0;
-        g.V = V;
-        g.ignore_index = prob->ignore_index;
-        g.M = (int32_t)M;
-        g.N = (int32_t)N;
-        g.d = (int32_t)d;
-        g.n_vt = (int32_t)ceil_div(M, ts.grad_bm);
-        if (!vpce::run_grad(prob->dtype, g, s)) return VP_ERR_HIP;
-
-        vpce::GemmArgs h;  // dH[t0 : t0+N] (+)= G^T W_chunk = G^T . (W^T)^T
-        h.A = strip_t;
-        h.lda = plan.Vc;
-        h.B = Wt;
-        h.ldb = plan.Vc;
-        h.C = dH + t0 * d;
-        h.ldc = d;
-        h.M = (int32_t)N;
-        h.N = (int32_t)d;
-        h.K = (int32_t)round_up(M, ts.kalign);  // G^T and W^T are zero past M
-        h.beta = first_vchunk ? 0 : 1;
-
-        vpce::GemmArgs w;  // dW_chunk (+)= G H[t0 : t0+N] = G . (H^T)^T
-        w.A = strip;
-        w.lda = plan.Tc;
-        w.B = (const char*)Ht + (size_t)t0 * eb;
-        w.ldb = plan.T_pad;
-        w.C = dWc;
-        w.ldc = d;
-        w.M = (int32_t)M;
-        w.N = (int32_t)d;
-        w.K = (int32_t)round_up(N, ts.kalign);  // G is zero past N
-        w.beta = (t0 > 0 || accumulate) ? 1 : 0;
-        if (!vpce::run_gemm_pair(prob->dtype, h, w, s)) return VP_ERR_HIP;
-      }
-      first_vchunk = false;
+      // dH[t0 : t0+N] (+)= G^T W_chunk = G^T . (W^T)^T
+      h.A = wsb + plan.off_gt[(k - 1) % 2];
+      h.lda = plan.Vc;
+      h.B = Wt;
+      h.ldb = plan.Vc;
+      h.C = dH + c.t0 * d;
+      h.ldc = d;
+      h.M = (int32_t)c.N;
+      h.N = (int32_t)d;
+      h.K = (int32_t)round_up(c.M, ts.kalign);  // G^T and W^T are zero past M
+      h.beta = c.first_vchunk ? 0 : 1;
+      // dW_chunk (+)= G H[t0 : t0+N] = G . (H^T)^T
+      w.A = wsb + plan.off_g[(k - 1) % 2];
+      w.lda = plan.Tc;
+      w.B = (const char*)Ht + (size_t)c.t0 * eb;
+      w.ldb = plan.T_pad;
+      w.C = dW_shards[c.q] + c.v0 * d;
+      w.ldc = d;
+      w.M = (int32_t)c.M;
+      w.N = (int32_t)d;
+      w.K = (int32_t)round_up(c.N, ts.kalign);  // G is zero past N
+      w.beta = (c.t0 > 0 || accumulate) ? 1 : 0;
     }
+    if (!vpce::run_bwd_stage(prob->dtype, h, w, g, s)) return VP_ERR_HIP;
   }
   return VP_OK;
 }

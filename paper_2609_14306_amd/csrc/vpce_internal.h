@@ -92,11 +92,17 @@ bool run_ws_init(unsigned long long* counter, hipStream_t s);
 bool run_fill_zero(float* p, int64_t n, hipStream_t s);
 bool run_fwd(int dtype, const FwdArgs& a, hipStream_t s);
 bool run_comb(const CombArgs& a, hipStream_t s);
-bool run_grad(int dtype, const GradArgs& a, hipStream_t s);
 bool run_count_bad(const int64_t* targets, int64_t T, int64_t V, int64_t ignore_index,
                    unsigned long long* counter, hipStream_t s);
-// Two independent GEMMs (the dH and dW contractions of one strip) in one launch.
-bool run_gemm_pair(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t s);
+// Per-XCD tile counts of one backward stage launch (dH, dW, residual tiles).
+struct StageSplit {
+  int32_t cnt[3][8], first[3][8];
+};
+
+// One backward stage: the dH (h) and dW (w) tiles of one strip and the residual
+// tiles (g) of the next strip, in one launch.  A kind with M == 0 is absent.
+bool run_bwd_stage(int dtype, const GemmArgs& h, const GemmArgs& w, const GradArgs& g,
+                   hipStream_t s);
 bool run_transpose(int dtype, const TransposeArgs& a, hipStream_t s);
 
 }  // namespace vpce

@@ -123,6 +123,8 @@ struct Gemm {
   using S = typename E::storage;
   static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
   static constexpr int NT = 64 * WGM * WGN;
+  static constexpr int OCC = 1;  // workgroups per CU the register budget is sized for
+  static constexpr int KDIV = 1;  // any K (ragged k-slices are zero-filled)
   static constexpr int WM = BM / WGM, WN = BN / WGN, MB = WM / 32, NB = WN / 32;
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be whole 32x32 blocks");
   using SA = Stage<E, BM, NT>;
@@ -216,20 +218,48 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
 }
 
-template <int BM_, int BN_, int WGM_, int WGN_, int STAGES = 4>
+#ifndef VPCE_DMA_STAGES
+#define VPCE_DMA_STAGES 2
+#endif
+#ifndef VPCE_DMA_ISSUE_AT
+#define VPCE_DMA_ISSUE_AT 1
+#endif
+// ISSUE_AT: k16 sub-step of a slice after whose MFMAs the refill loads are issued
+// (0: before the first sub-step's LDS reads).
+#ifndef VPCE_DMA_BK
+#define VPCE_DMA_BK 64
+#endif
+template <int BM_, int BN_, int WGM_, int WGN_, int STAGES = VPCE_DMA_STAGES,
+          int ISSUE_AT = VPCE_DMA_ISSUE_AT, int BK_ = VPCE_DMA_BK, int OCC_ = 0>
 struct GemmDma {
   using S = uint16_t;
   static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
   static constexpr int NT = 64 * WGM * WGN, NWAVES = WGM * WGN;
+  // Workgroups per CU the register budget is sized for (default: two wavefronts
+  // per SIMD in total).
+  static constexpr int OCC = OCC_ ? OCC_ : 512 / NT;
   static constexpr int WM = BM / WGM, WN = BN / WGN, MB = WM / 32, NB = WN / 32;
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be whole 32x32 blocks");
-  static constexpr int BK = 32;
+  static constexpr int BK = BK_;
+  static_assert(BK == 32 || BK == 64, "slice depth");
+  static constexpr int KDIV = BK;  // K must be a multiple of the slice depth
+  static constexpr int CPR = BK / 8;              // 16-byte chunks per row
+  static constexpr int ROW_BYTES = BK * 2;
+  static constexpr int RPW = 256 / ROW_BYTES;     // rows per 64-bank (256-byte) window
+  static constexpr int RPI = 1024 / ROW_BYTES;    // rows per 1 KiB load instruction
   static constexpr int ROWS = BM + BN;            // rows of one slice (A then B)
-  static constexpr int SLICE_BYTES = ROWS * 64;
-  static constexpr int GROUPS = ROWS / 16;        // 1 KiB load instructions per slice
-  static_assert(ROWS % 16 == 0, "slice rows");
+  static constexpr int SLICE_BYTES = ROWS * ROW_BYTES;
+  static constexpr int GROUPS = ROWS / RPI;       // load instructions per slice
+  static_assert(ROWS % RPI == 0, "slice rows");
   static constexpr int G_LO = GROUPS / NWAVES, G_REM = GROUPS % NWAVES;  // waves < G_REM do one more
   static constexpr int LDS_ELEMS = STAGES * SLICE_BYTES / 2;
+  static_assert(STAGES >= 2, "ring depth");
+
+  // Chunk c of slice row r lives in slot c ^ key(r): within one 256-byte window
+  // the rows sit at distinct offsets, and key(r) differs for the CPR rows that
+  // share a window offset, so a read phase of 16 consecutive rows at one chunk
+  // touches 16 distinct 4-bank groups.
+  __device__ __forceinline__ static int key(int r) { return (r / RPW) % CPR; }
 
   __device__ __forceinline__ static int wave_m(int wave) { return (wave / WGN) * WM; }
   __device__ __forceinline__ static int wave_n(int wave) { return (wave % WGN) * WN; }
@@ -240,13 +270,13 @@ struct GemmDma {
                                                int kt, int nk, uint32_t lds0, int wave, int lane) {
     const int kc = min(kt, nk - 1) * BK;  // past the end: reload the last slice (never read)
     const uint32_t slot_base = lds0 + (uint32_t)((kt % STAGES) * SLICE_BYTES);
-    const int row_in = lane >> 2;         // 16 rows per instruction, 4 lanes per row
+    const int row_in = lane / CPR;        // RPI rows per instruction, CPR lanes per row
 #pragma unroll
     for (int q = 0; q < G_LO + 1; ++q) {
       if (q == G_LO && wave >= G_REM) break;
       const int g = wave + q * NWAVES;
-      const int r = g * 16 + row_in;    // row within the slice
-      const int chunk = (lane & 3) ^ ((r >> 2) & 3);
+      const int r = g * RPI + row_in;   // row within the slice
+      const int chunk = (lane % CPR) ^ key(r);
       const S* src;
       if (r < BM) {
         src = A + (int64_t)min(m0 + r, M - 1) * lda + kc + 8 * chunk;
@@ -258,7 +288,7 @@ struct GemmDma {
   }
 
   __device__ __forceinline__ static bf16x8_t frag(const S* slot, int row, int chunk) {
-    return *(const bf16x8_t*)(slot + row * 32 + ((chunk ^ ((row >> 2) & 3)) << 3));
+    return *(const bf16x8_t*)(slot + row * BK + ((chunk ^ key(row)) << 3));
   }
 
   __device__ __forceinline__ static void run(f32x16_t (&acc)[MB][NB], const S* __restrict__ A,
@@ -282,11 +312,11 @@ struct GemmDma {
         wait_vmcnt<(STAGES - 2) * G_LO>();
       __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS reads of the last slice are done
       __builtin_amdgcn_s_barrier();
-      // slot (kt-1) % STAGES is free now: refill it with slice kt + STAGES - 1
-      issue(A, lda, m0, M, B, ldb, n0, N, kt + STAGES - 1, nk, lds0, wave, lane);
       const S* slot = smem + (kt % STAGES) * (SLICE_BYTES / 2);
 #pragma unroll
       for (int kk = 0; kk < BK / 16; ++kk) {
+        // slot (kt-1) % STAGES is free since the barrier: refill it with slice kt + STAGES - 1
+        if (kk == ISSUE_AT) issue(A, lda, m0, M, B, ldb, n0, N, kt + STAGES - 1, nk, lds0, wave, lane);
         bf16x8_t a[MB], b[NB];
         const int chunk = 2 * kk + (lane >> 5);
 #pragma unroll
@@ -356,7 +386,7 @@ __global__ void fill_zero_kernel(float* p, int64_t n) {
 // per-lane online-softmax state, gathers the target logit from the one tile
 // whose rows contain it, and writes its partial (m, s) per token.
 template <class E, class G>
-__global__ void __launch_bounds__(G::NT) fwd_kernel(FwdArgs a) {
+__global__ void __launch_bounds__(G::NT, G::OCC) fwd_kernel(FwdArgs a) {
   using S = typename E::storage;
   constexpr int BM = G::BM, BN = G::BN, MB = G::MB, NB = G::NB;
   __shared__ __attribute__((aligned(16))) S smem[G::LDS_ELEMS];
@@ -504,14 +534,12 @@ __global__ void __launch_bounds__(256) comb_kernel(CombArgs a) {
 // fall outside the chunk are written as zeros so that both contractions can
 // read whole 16-byte chunks past a ragged edge.
 template <class E, class G>
-__global__ void __launch_bounds__(G::NT) grad_kernel(GradArgs a) {
+__device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
+                                          typename E::storage* smem) {
   using S = typename E::storage;
   constexpr int BM = G::BM, BN = G::BN, MB = G::MB, NB = G::NB;
-  __shared__ __attribute__((aligned(16))) S smem[G::LDS_ELEMS];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = G::wave_m(wave), wn = G::wave_n(wave);
-  int vt, tb;
-  grouped_tile(xcd_logical(blockIdx.x, gridDim.x), a.n_vt, gridDim.x / a.n_vt, 4, vt, tb);
   const int m0 = vt * BM, n0 = tb * BN;
 
   f32x16_t acc[MB][NB];
@@ -615,29 +643,39 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int nt,
     }
 }
 
-// Per-XCD split of a two-problem grid: XCD x runs cnt0[x] tiles of problem 0
-// (numbered from first0[x]) and then its share of problem 1 (from first1[x]), so
-// that every XCD gets an even share of both problems and consecutive tiles of
-// one problem stay on one XCD's L2.
-struct PairSplit {
-  int32_t cnt0[8], first0[8], first1[8];
-};
-
-template <class E, class G>
-__global__ void __launch_bounds__(G::NT) gemm_pair_kernel(GemmArgs a0, GemmArgs a1, PairSplit sp) {
+// One launch of the backward pipeline: the dH and dW tiles of strip c and
+// the residual tiles of strip c+1 (which writes the other strip buffer).  XCD x
+// runs cnt[0][x] dH tiles, then cnt[1][x] dW tiles, then cnt[2][x] residual
+// tiles (numbered from first[.][x]): every XCD gets an even share of each kind,
+// consecutive tiles of one kind stay on one XCD's L2, and the longest tiles go
+// first so that the partly filled last round is made of the short ones.
+template <class E, class GL, class GM>
+__global__ void __launch_bounds__(GM::NT, GM::OCC)
+    bwd_stage_kernel(GemmArgs h, GemmArgs w, GradArgs g, StageSplit sp) {
+  static_assert(GL::NT == GM::NT, "one workgroup size for every tile kind");
   using S = typename E::storage;
-  __shared__ __attribute__((aligned(16))) S smem[G::LDS_ELEMS];
-  const int xcd = blockIdx.x % 8, local = blockIdx.x / 8;
+  constexpr int LDS = GL::LDS_ELEMS > GM::LDS_ELEMS ? GL::LDS_ELEMS : GM::LDS_ELEMS;
+  __shared__ __attribute__((aligned(16))) S smem[LDS];
+  const int xcd = blockIdx.x % 8;
+  int local = blockIdx.x / 8;
   int mt, nt;
-  if (local < sp.cnt0[xcd]) {
-    const int n_n = (a0.N + G::BN - 1) / G::BN, n_m = (a0.M + G::BM - 1) / G::BM;
-    grouped_tile(sp.first0[xcd] + local, n_m, n_n, 4, mt, nt);
-    gemm_tile<E, G>(a0, mt, nt, smem);
-  } else {
-    const int n_n = (a1.N + G::BN - 1) / G::BN, n_m = (a1.M + G::BM - 1) / G::BM;
-    grouped_tile(sp.first1[xcd] + local - sp.cnt0[xcd], n_m, n_n, 4, mt, nt);
-    gemm_tile<E, G>(a1, mt, nt, smem);
+  if (local < sp.cnt[0][xcd]) {
+    const int n_n = (h.N + GM::BN - 1) / GM::BN, n_m = (h.M + GM::BM - 1) / GM::BM;
+    grouped_tile(sp.first[0][xcd] + local, n_m, n_n, 4, mt, nt);
+    gemm_tile<E, GM>(h, mt, nt, smem);
+    return;
   }
+  local -= sp.cnt[0][xcd];
+  if (local < sp.cnt[1][xcd]) {
+    const int n_n = (w.N + GM::BN - 1) / GM::BN, n_m = (w.M + GM::BM - 1) / GM::BM;
+    grouped_tile(sp.first[1][xcd] + local, n_m, n_n, 4, mt, nt);
+    gemm_tile<E, GM>(w, mt, nt, smem);
+    return;
+  }
+  local -= sp.cnt[1][xcd];
+  const int n_tb = (g.N + GL::BN - 1) / GL::BN;
+  grouped_tile(sp.first[2][xcd] + local, g.n_vt, n_tb, 4, mt, nt);
+  grad_tile<E, GL>(g, mt, nt, smem);
 }
 
 // out[c][r] = in[r][c] through a 64 x 64 LDS tile; rows R..R_pad-1 of the
@@ -669,12 +707,29 @@ __global__ void __launch_bounds__(256) transpose_kernel(TransposeArgs a) {
 //            (d = 2880 = 15 x 192), else 256 x 256 (waves 2 x 4)
 // f32: 64 x 64 tiles, 256 threads (waves 2 x 2), register-staged.
 template <class E> struct Cfg;
+#ifndef VPCE_TILESET
+#define VPCE_TILESET 1
+#endif
 template <> struct Cfg<Bf16> {
+#if VPCE_TILESET == 1
   using Logits = GemmDma<256, 256, 2, 4>;
-  using LogitsReg = Gemm<Bf16, 256, 256, 2, 4>;
   using MmA = GemmDma<256, 256, 2, 4>;
   using MmB = GemmDma<256, 192, 4, 2>;
-  static constexpr int KALIGN = 32;  // K granularity the dH / dW launches need
+#elif VPCE_TILESET == 3
+  // one 256-thread workgroup per CU, 128 x 128 (logits) / 128 x 96 wave tiles
+  using Logits = GemmDma<256, 256, 2, 2, VPCE_DMA_STAGES, VPCE_DMA_ISSUE_AT, VPCE_DMA_BK, 1>;
+  using MmA = GemmDma<256, 256, 2, 2, VPCE_DMA_STAGES, VPCE_DMA_ISSUE_AT, VPCE_DMA_BK, 1>;
+  using MmB = GemmDma<256, 192, 2, 2, VPCE_DMA_STAGES, VPCE_DMA_ISSUE_AT, VPCE_DMA_BK, 1>;
+#else
+  // 256-thread workgroups, two per CU: one workgroup's barrier stalls overlap the
+  // other's MFMAs.  Per-wave tiles stay 128 x 64 (logits) and 64 x 96 (dH / dW).
+  using Logits = GemmDma<256, 128, 2, 2, 3>;
+  using MmA = GemmDma<256, 128, 2, 2, 3>;
+  using MmB = GemmDma<128, 192, 2, 2, 3>;
+#endif
+  using LogitsReg = Gemm<Bf16, Logits::BM, Logits::BN, Logits::WGM, Logits::WGN>;
+  static_assert(64 % MmA::KDIV == 0 && 64 % MmB::KDIV == 0, "dH / dW launch granularity");
+  static constexpr int KALIGN = 64;  // K granularity the dH / dW launches need
 };
 template <> struct Cfg<F32> {
   using Logits = Gemm<F32, 64, 64, 2, 2>;
@@ -694,48 +749,71 @@ static bool launch_fwd_g(const FwdArgs& a, hipStream_t s) {
 }
 template <class E>
 static bool launch_fwd(const FwdArgs& a, hipStream_t s) {
-  if (a.d % 32 == 0) return launch_fwd_g<E, typename Cfg<E>::Logits>(a, s);
+  if (a.d % Cfg<E>::Logits::KDIV == 0) return launch_fwd_g<E, typename Cfg<E>::Logits>(a, s);
   return launch_fwd_g<E, typename Cfg<E>::LogitsReg>(a, s);
 }
-template <class E, class G>
-static bool launch_grad_g(const GradArgs& a, hipStream_t s) {
-  const unsigned grid = (unsigned)(a.n_vt * ((a.N + G::BN - 1) / G::BN));
-  hipLaunchKernelGGL((grad_kernel<E, G>), dim3(grid), dim3(G::NT), 0, s, a);
-  return launched_ok();
-}
-template <class E>
-static bool launch_grad(const GradArgs& a, hipStream_t s) {
-  if (a.d % 32 == 0) return launch_grad_g<E, typename Cfg<E>::Logits>(a, s);
-  return launch_grad_g<E, typename Cfg<E>::LogitsReg>(a, s);
-}
-template <class E, class G>
-static bool launch_pair_tiles(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
-  const int t0 = a0.M > 0 ? ((a0.M + G::BM - 1) / G::BM) * ((a0.N + G::BN - 1) / G::BN) : 0;
-  const int t1 = a1.M > 0 ? ((a1.M + G::BM - 1) / G::BM) * ((a1.N + G::BN - 1) / G::BN) : 0;
-  const int n = t0 + t1;
-  if (n == 0) return true;
-  // workgroup b runs on XCD b % 8: XCD x receives n/8 (+1 for x < n%8) of them
-  PairSplit sp;
-  int f0 = 0, f1 = 0;
-  for (int x = 0; x < 8; ++x) {
-    const int cnt = n / 8 + (x < n % 8 ? 1 : 0);
-    const int c0 = t0 / 8 + (x < t0 % 8 ? 1 : 0);  // <= cnt (see the argument below)
-    sp.cnt0[x] = c0;
-    sp.first0[x] = f0;
-    sp.first1[x] = f1;
-    f0 += c0;
-    f1 += cnt - c0;
+// Per-XCD split of n0 + n1 + n2 workgroups (workgroup b runs on XCD b % 8, so
+// XCD x receives n/8 of them, one more for x < n%8): kinds 0 and 1 are spread
+// as evenly as the capacity allows, kind 2 takes the rest.
+static StageSplit split_stage(const int n_kind[3]) {
+  StageSplit sp;
+  const int n = n_kind[0] + n_kind[1] + n_kind[2];
+  int cap[8];
+  for (int x = 0; x < 8; ++x) cap[x] = n / 8 + (x < n % 8 ? 1 : 0);
+  for (int t = 0; t < 2; ++t) {
+    int give = n_kind[t];
+    for (int x = 0; x < 8; ++x) {
+      const int c = std::min(cap[x], n_kind[t] / 8);
+      sp.cnt[t][x] = c;
+      cap[x] -= c;
+      give -= c;
+    }
+    for (int x = 0; give > 0; x = (x + 1) % 8)
+      if (cap[x] > 0) {
+        ++sp.cnt[t][x];
+        --cap[x];
+        --give;
+      }
   }
-  // c0 <= cnt: if n/8 > t0/8 this is immediate; if they are equal then n%8 >= t0%8.
-  hipLaunchKernelGGL((gemm_pair_kernel<E, G>), dim3((unsigned)n), dim3(G::NT), 0, s, a0, a1, sp);
+  for (int x = 0; x < 8; ++x) sp.cnt[2][x] = cap[x];
+  for (int t = 0; t < 3; ++t) {
+    int f = 0;
+    for (int x = 0; x < 8; ++x) {
+      sp.first[t][x] = f;
+      f += sp.cnt[t][x];
+    }
+  }
+  return sp;
+}
+
+template <class E, class GL, class GM>
+static bool launch_stage_g(const GemmArgs& h, const GemmArgs& w, const GradArgs& g, hipStream_t s) {
+  auto tiles = [](const GemmArgs& a, int bm, int bn) {
+    return a.M > 0 ? ((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn) : 0;
+  };
+  int n_kind[3];
+  n_kind[0] = tiles(h, GM::BM, GM::BN);
+  n_kind[1] = tiles(w, GM::BM, GM::BN);
+  n_kind[2] = g.M > 0 ? g.n_vt * ((g.N + GL::BN - 1) / GL::BN) : 0;
+  const int n = n_kind[0] + n_kind[1] + n_kind[2];
+  if (n == 0) return true;
+  const StageSplit sp = split_stage(n_kind);
+  hipLaunchKernelGGL((bwd_stage_kernel<E, GL, GM>), dim3((unsigned)n), dim3(GM::NT), 0, s, h, w,
+                     g, sp);
   return launched_ok();
 }
+template <class E, class GL>
+static bool launch_stage_l(const GemmArgs& h, const GemmArgs& w, const GradArgs& g, hipStream_t s) {
+  // dH and dW share N (= d)
+  const int N = h.M > 0 ? h.N : w.N;
+  if (N % 256 != 0 && N % 192 == 0)
+    return launch_stage_g<E, GL, typename Cfg<E>::MmB>(h, w, g, s);
+  return launch_stage_g<E, GL, typename Cfg<E>::MmA>(h, w, g, s);
+}
 template <class E>
-static bool launch_pair(const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
-  // both problems share N (= d)
-  if (a0.N % 256 != 0 && a0.N % 192 == 0)
-    return launch_pair_tiles<E, typename Cfg<E>::MmB>(a0, a1, s);
-  return launch_pair_tiles<E, typename Cfg<E>::MmA>(a0, a1, s);
+static bool launch_stage(const GemmArgs& h, const GemmArgs& w, const GradArgs& g, hipStream_t s) {
+  if (g.d % Cfg<E>::Logits::KDIV == 0) return launch_stage_l<E, typename Cfg<E>::Logits>(h, w, g, s);
+  return launch_stage_l<E, typename Cfg<E>::LogitsReg>(h, w, g, s);
 }
 
 // ---- entry points used by the host API (vpce_api.cpp) ----
@@ -774,9 +852,6 @@ bool run_comb(const CombArgs& a, hipStream_t s) {
   hipLaunchKernelGGL(comb_kernel, dim3(grid), dim3(256), 0, s, a);
   return launched_ok();
 }
-bool run_grad(int dtype, const GradArgs& a, hipStream_t s) {
-  return dtype == 1 ? launch_grad<Bf16>(a, s) : launch_grad<F32>(a, s);
-}
 bool run_count_bad(const int64_t* targets, int64_t T, int64_t V, int64_t ignore_index,
                    unsigned long long* counter, hipStream_t s) {
   if (T <= 0) return true;
@@ -784,8 +859,9 @@ bool run_count_bad(const int64_t* targets, int64_t T, int64_t V, int64_t ignore_
                      T, V, ignore_index, counter);
   return launched_ok();
 }
-bool run_gemm_pair(int dtype, const GemmArgs& a0, const GemmArgs& a1, hipStream_t s) {
-  return dtype == 1 ? launch_pair<Bf16>(a0, a1, s) : launch_pair<F32>(a0, a1, s);
+bool run_bwd_stage(int dtype, const GemmArgs& h, const GemmArgs& w, const GradArgs& g,
+                   hipStream_t s) {
+  return dtype == 1 ? launch_stage<Bf16>(h, w, g, s) : launch_stage<F32>(h, w, g, s);
 }
 bool run_transpose(int dtype, const TransposeArgs& a, hipStream_t s) {
   if (a.C <= 0 || a.R_pad <= 0) return true;
