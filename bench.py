@@ -9,8 +9,9 @@ the C ABI on torch's current stream, inputs resident in HBM.
 Prints ONE JSON line: tokens/s of the whole job (value), ms per step, achieved
 TFLOP/s counted as 8*T*V*d per step (2TVd forward, 6TVd backward with recompute)
 against the dense bf16 MFMA peak, the working set, a roofline entry for the
-fused forward kernel (timed with HIP events on the launch stream) and the CPU
-oracle timed on a bounded row sample of the same workload.
+backward stage kernel (the dominant one) and one for the fused forward kernel,
+both timed with HIP events on the launch stream, and the CPU oracle timed on a
+bounded row sample of the same workload.
 """
 from __future__ import annotations
 
@@ -36,11 +37,41 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--cpu-sample-rows", type=int, default=256,
+    ap.add_argument("--cpu-sample-rows", type=int, default=2048,
                     help="token rows of the workload the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--strip-elems", type=int, default=0)
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
+                    help="only run one device-to-device copy of BYTES (for scaling HBM counters)")
     return ap.parse_args()
+
+
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_14306_amd", "csrc", "vpce_kernels.hip")
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_longctx_T32768_d2880_V201088.md")
+
+
+def kernel_source_sha256() -> str:
+    import hashlib
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed counter profile, or None when the
+    profile is missing, covers another workload, or the kernels changed since it was taken."""
+    try:
+        lines = open(TRAFFIC_PROFILE).read().splitlines()
+    except OSError:
+        return None
+    vals = {}
+    for ln in lines:
+        if ln.startswith("- ") and ":" in ln:
+            k, v = ln[2:].split(":", 1)
+            vals[k.strip()] = v.strip().strip("`")
+    if vals.get("workload") != workload or vals.get("kernel_source_sha256") != kernel_source_sha256():
+        return None
+    key = f"{kernel}_hbm_bytes_per_launch"
+    return float(vals[key]) if key in vals else None
 
 
 def cpu_baseline(inp, rows: int):
@@ -84,6 +115,15 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
+    if args.copy_calibration:
+        n = args.copy_calibration // 4
+        src = torch.ones(n, dtype=torch.float32, device=dev)
+        dst = torch.empty_like(src)
+        torch.cuda.synchronize()
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": n * 4}), flush=True)
+        return
     w = wl.WORKLOADS[args.workload]
     t_gen = time.perf_counter()
     inp = wl.make_inputs(w)
@@ -143,8 +183,11 @@ def main():
     tflops = flops / (ms_per_step * 1e-3) / 1e12
     peak = PEAK_BF16_TFLOPS if inp.dtype == "bf16" else PEAK_F32_TFLOPS
     fwd_avg = float(np.mean(fwd_ms))
+    bwd_avg = float(np.mean(bwd_ms))
     fwd_tflops = 2.0 * T * V * d / (fwd_avg * 1e-3) / 1e12
-
+    bwd_tflops = 6.0 * T * V * d / (bwd_avg * 1e-3) / 1e12
+    bwd_traffic = measured_traffic("bwd_stage_kernel", w.name)
+    fwd_traffic = measured_traffic("fwd_kernel", w.name)
     out = {
         "metric": "vocab-proj CE fwd+bwd tokens/s; % bf16 MFMA peak; peak working set MiB",
         "value": T / (ms_per_step * 1e-3),
@@ -164,13 +207,20 @@ def main():
         "tflops": tflops,
         "pct_peak": 100.0 * tflops / peak,
         "fwd_ms": fwd_avg,
-        "bwd_ms": float(np.mean(bwd_ms)),
+        "bwd_ms": bwd_avg,
         "working_set_mib": {"workspace_fwd": fwd_b / 2**20, "workspace_bwd": bwd_b / 2**20,
                             "allocated_during_steps": extra_alloc / 2**20,
                             "peak_over_resident": (max(fwd_b, bwd_b) + extra_alloc) / 2**20},
-        "roofline": {"kernel": "fwd_kernel (fused logits tiles + online LSE fold)",
-                     "bound": "mfma", "achieved": fwd_tflops, "peak": peak, "unit": "TFLOP/s",
-                     "frac": fwd_tflops / peak, "traffic": None},
+        # The dominant kernel by time: the backward stage kernel (recompute + residual,
+        # dH and dW tiles), launched once per strip plus once; achieved = 6TVd over the
+        # backward call's event time (which also holds ~1% of transposes), i.e. the
+        # average flops per launch over the average launch duration.
+        "roofline": {"kernel": "bwd_stage_kernel (logits recompute + residual + dH + dW MFMA tiles)",
+                     "bound": "mfma", "achieved": bwd_tflops, "peak": peak, "unit": "TFLOP/s",
+                     "frac": bwd_tflops / peak, "traffic": bwd_traffic},
+        "roofline_fwd": {"kernel": "fwd_kernel (fused logits tiles + online LSE fold)",
+                         "bound": "mfma", "achieved": fwd_tflops, "peak": peak, "unit": "TFLOP/s",
+                         "frac": fwd_tflops / peak, "traffic": fwd_traffic},
         "bad_targets": bad,
         "input_gen_s": t_gen,
     }

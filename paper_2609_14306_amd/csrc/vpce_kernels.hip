@@ -699,34 +699,18 @@ __global__ void __launch_bounds__(256) transpose_kernel(TransposeArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tile configurations.  bf16: 512 threads (two wavefronts per SIMD, so one
-// wave's waits overlap the other's MFMAs), direct-to-LDS 4-slice ring.
-//   logits (forward / recompute): 256 vocabulary rows x 256 tokens, waves 2 x 4
-//     (register-staged double buffer when d is not a multiple of 32)
-//   dH / dW: 256 x 192 (waves 4 x 2) when d is a multiple of 192 but not of 256
-//            (d = 2880 = 15 x 192), else 256 x 256 (waves 2 x 4)
-// f32: 64 x 64 tiles, 256 threads (waves 2 x 2), register-staged.
+// Tile configurations.  bf16: the direct-to-LDS ring (BK = 64, two slots); the
+// register-staged tile when d is not a multiple of 64.  f32: 64 x 64 tiles,
+// 256 threads (waves 2 x 2), register-staged.
 template <class E> struct Cfg;
-#ifndef VPCE_TILESET
-#define VPCE_TILESET 1
-#endif
 template <> struct Cfg<Bf16> {
-#if VPCE_TILESET == 1
+  // 512-thread workgroups (two wavefronts per SIMD), 256 x 256 tiles, 128 x 64 per
+  // wave, for every contraction (d = 2880 pads the dH / dW column tiles to 3072:
+  // measured faster inside the backward stage launch than 256 x 192 tiles with
+  // 64 x 96 per wave, whose fragment reads per MFMA are higher).
   using Logits = GemmDma<256, 256, 2, 4>;
   using MmA = GemmDma<256, 256, 2, 4>;
-  using MmB = GemmDma<256, 192, 4, 2>;
-#elif VPCE_TILESET == 3
-  // one 256-thread workgroup per CU, 128 x 128 (logits) / 128 x 96 wave tiles
-  using Logits = GemmDma<256, 256, 2, 2, VPCE_DMA_STAGES, VPCE_DMA_ISSUE_AT, VPCE_DMA_BK, 1>;
-  using MmA = GemmDma<256, 256, 2, 2, VPCE_DMA_STAGES, VPCE_DMA_ISSUE_AT, VPCE_DMA_BK, 1>;
-  using MmB = GemmDma<256, 192, 2, 2, VPCE_DMA_STAGES, VPCE_DMA_ISSUE_AT, VPCE_DMA_BK, 1>;
-#else
-  // 256-thread workgroups, two per CU: one workgroup's barrier stalls overlap the
-  // other's MFMAs.  Per-wave tiles stay 128 x 64 (logits) and 64 x 96 (dH / dW).
-  using Logits = GemmDma<256, 128, 2, 2, 3>;
-  using MmA = GemmDma<256, 128, 2, 2, 3>;
-  using MmB = GemmDma<128, 192, 2, 2, 3>;
-#endif
+  using MmB = MmA;
   using LogitsReg = Gemm<Bf16, Logits::BM, Logits::BN, Logits::WGM, Logits::WGN>;
   static_assert(64 % MmA::KDIV == 0 && 64 % MmB::KDIV == 0, "dH / dW launch granularity");
   static constexpr int KALIGN = 64;  // K granularity the dH / dW launches need
