@@ -51,7 +51,9 @@ extern "C" {
 typedef enum {
   VP_OK = 0,
   VP_ERR_NULL = 1,        /* a required pointer is NULL */
-  VP_ERR_SHAPE = 2,       /* T < 0, d < 1, P out of [1, VP_MAX_SHARDS], V_p < 0, sum V_p < 1, d % 8 != 0 */
+  VP_ERR_SHAPE = 2,       /* T out of [0, 2^23 - 256], d out of [8, 2^22] or d % 8 != 0,
+                             P out of [1, VP_MAX_SHARDS], V_p out of [0, 2^30], sum V_p out of
+                             [1, 2^31 - 1], strip_elems out of [0, 2^30] */
   VP_ERR_DTYPE = 3,       /* dtype is not VP_F32 / VP_BF16 */
   VP_ERR_ORDER = 4,       /* order is not a permutation of 0..P-1 */
   VP_ERR_ALIGN = 5,       /* a device pointer is not 16-byte aligned */
@@ -73,8 +75,8 @@ typedef enum {
                                weight shard and collects every rank's contribution */
 
 typedef struct {
-  int64_t T;                  /* local tokens, >= 0 (T == 0 is a no-op) */
-  int64_t d;                  /* hidden width, >= 8 and a multiple of 8 */
+  int64_t T;                  /* local tokens, 0..2^23 - 256 (T == 0 is a no-op) */
+  int64_t d;                  /* hidden width, 8..2^22 and a multiple of 8 */
   int32_t P;                  /* number of vocabulary shards, 1..VP_MAX_SHARDS */
   int32_t dtype;              /* vp_dtype of H and W */
   const int64_t* shard_rows;  /* host [P]: V_p >= 0 rows of shard p, sum >= 1 */

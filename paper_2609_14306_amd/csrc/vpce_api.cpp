@@ -26,11 +26,17 @@ inline int64_t ceil_div(int64_t x, int64_t m) { return (x + m - 1) / m; }
 
 size_t elem_bytes(int dtype) { return dtype == VP_BF16 ? 2 : 4; }
 
+constexpr int64_t kMaxT = (1ll << 23) - 256;
+constexpr int64_t kMaxD = 1ll << 22;
+
 vp_status validate(const vp_problem* p, int64_t* V_out) {
   if (!p) return VP_ERR_NULL;
   if (p->dtype != VP_F32 && p->dtype != VP_BF16) return VP_ERR_DTYPE;
-  if (p->T < 0 || p->d < 8 || p->d % 8 != 0 || p->d > (1ll << 30)) return VP_ERR_SHAPE;
-  if (p->T > (1ll << 30)) return VP_ERR_SHAPE;
+  // The bf16 GEMM tiles address a 256-row operand tile with 32-bit byte offsets
+  // (256 rows x leading dimension x 2 bytes < 2^32): leading dimensions are d,
+  // the padded token count and strip widths, so T and d are capped below 2^23.
+  if (p->T < 0 || p->d < 8 || p->d % 8 != 0 || p->d > kMaxD) return VP_ERR_SHAPE;
+  if (p->T > kMaxT) return VP_ERR_SHAPE;
   if (p->P < 1 || p->P > VP_MAX_SHARDS) return VP_ERR_SHAPE;
   if (!p->shard_rows) return VP_ERR_NULL;
   if (p->strip_elems < 0 || p->strip_elems > (1ll << 30)) return VP_ERR_SHAPE;

@@ -192,23 +192,52 @@ struct Gemm {
 // ---------------------------------------------------------------------------
 // bf16 tile GEMM fed by direct global -> LDS loads (global_load_lds_dwordx4,
 // 16 bytes per lane straight into LDS, no staging registers) through a ring of
-// STAGES k-slices of BK = 32, so that STAGES-1 slices are in flight while one
-// is multiplied.  Requires K to be a multiple of 32 and both operands to hold
-// finite values up to that K (the backward's buffers are zero-padded).
+// two k-slices of BK = 64.  Requires K to be a multiple of 64 and both operands
+// to hold finite values up to that K (the backward's buffers are zero-padded).
 //
-// LDS slice layout: the A rows then the B rows, 64 bytes (four 16-byte chunks)
-// per row, chunk c of row r stored in slot c ^ ((r >> 2) & 3): the 16 lanes of
-// one LDS read phase (16 consecutive rows, same chunk) then hit 16 distinct
-// 4-bank groups, and each load instruction writes 1 KiB contiguously (16 rows).
+// LDS slice layout: the A rows then the B rows, 128 bytes (eight 16-byte
+// chunks) per row, chunk c of row r stored in slot c ^ ((r >> 1) & 7): the 16
+// lanes of one LDS read phase (16 consecutive rows, same chunk) hit 16 distinct
+// 4-bank groups, and each load instruction writes 1 KiB contiguously (8 rows).
 //
-// The loads are issued from inline assembly so that the compiler, which cannot
-// tell which ring slot an LDS read touches, does not drain every load in flight
-// before each read; completion is tracked by hand: before the barrier that
-// opens slice kt, a wave waits until only the loads of the STAGES-2 younger
-// slices are outstanding (loads return in issue order).  Slices past the end
-// are loaded anyway (a clamped, valid address) so the count stays constant.
-__device__ __forceinline__ void lds_dma16(const void* gsrc, uint32_t lds_byte_addr) {
-  asm volatile("global_load_lds_dwordx4 %0, off" ::"v"(gsrc), "{m0}"(lds_byte_addr) : "memory");
+// Schedule of one wave (slice kt lives in ring slot kt & 1; sub-step kk covers
+// k = 16 kk .. 16 kk + 15 of the slice):
+//   sub-steps 0..2: read the fragments of sub-step kk+1 into the spare register
+//                   set, then issue the MFMAs of sub-step kk;
+//   sub-step 3:     wait for this wave's loads of slice kt+1, barrier, issue the
+//                   loads of slice kt+2 into slot kt & 1 (every wave finished
+//                   reading slice kt before the barrier), read the fragments of
+//                   slice kt+1 sub-step 0, then issue the MFMAs of sub-step 3.
+// The MFMAs never wait on an LDS read issued in the same sub-step, the only
+// barrier of a slice sits where every wave still holds a sub-step of MFMAs in
+// registers, and each slice's loads have a whole slice of MFMAs to land.
+//
+// The loads are issued from inline assembly with a scalar base (the tile's
+// first row at the slice's k offset) and a 32-bit per-lane byte offset, so that
+// the compiler neither drains the loads before each LDS read (it cannot tell
+// which ring slot a read touches) nor keeps 64-bit addresses per load.
+// Completion is tracked by hand with vmcnt: loads return in issue order and the
+// only loads a wave has in flight are its slice loads.
+// Four loads from one scalar base into four LDS destinations, as one asm block
+// so that nothing the compiler schedules can land between them.  The hazards
+// the compiler's hazard recognizer cannot see inside inline assembly are
+// covered here: five wait states before the first load in case a VALU
+// instruction (v_readlane of a spilled value, a carry-out) wrote the base
+// SGPRs just before the block, and one after each M0 write, which an LDS DMA
+// reads.
+__device__ __forceinline__ void lds_dma16x4(const void* sbase, uint32_t o0, uint32_t o1,
+                                            uint32_t o2, uint32_t o3, uint32_t l0, uint32_t l1,
+                                            uint32_t l2, uint32_t l3) {
+  uint32_t m0v = l0;  // M0 is an operand (not a clobber): the compiler knows the block writes it
+  asm volatile(
+      "s_nop 4\n\t"
+      "s_nop 0\n\tglobal_load_lds_dwordx4 %1, %5\n\t"
+      "s_mov_b32 m0, %6\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %5\n\t"
+      "s_mov_b32 m0, %7\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %3, %5\n\t"
+      "s_mov_b32 m0, %8\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %4, %5"
+      : "+{m0}"(m0v)
+      : "v"(o0), "v"(o1), "v"(o2), "v"(o3), "s"(sbase), "s"(l1), "s"(l2), "s"(l3)
+      : "memory");
 }
 
 template <int N>
@@ -217,43 +246,29 @@ __device__ __forceinline__ void wait_vmcnt() {
   // s_waitcnt simm16 on gfx9: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14
   __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
 }
+__device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
-#ifndef VPCE_DMA_STAGES
-#define VPCE_DMA_STAGES 2
-#endif
-#ifndef VPCE_DMA_ISSUE_AT
-#define VPCE_DMA_ISSUE_AT 1
-#endif
-// ISSUE_AT: k16 sub-step of a slice after whose MFMAs the refill loads are issued
-// (0: before the first sub-step's LDS reads).
-#ifndef VPCE_DMA_BK
-#define VPCE_DMA_BK 64
-#endif
-template <int BM_, int BN_, int WGM_, int WGN_, int STAGES = VPCE_DMA_STAGES,
-          int ISSUE_AT = VPCE_DMA_ISSUE_AT, int BK_ = VPCE_DMA_BK, int OCC_ = 0>
+template <int BM_, int BN_, int WGM_, int WGN_>
 struct GemmDma {
   using S = uint16_t;
   static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
   static constexpr int NT = 64 * WGM * WGN, NWAVES = WGM * WGN;
-  // Workgroups per CU the register budget is sized for (default: two wavefronts
-  // per SIMD in total).
-  static constexpr int OCC = OCC_ ? OCC_ : 512 / NT;
+  static constexpr int OCC = 512 / NT;  // two wavefronts per SIMD in total
   static constexpr int WM = BM / WGM, WN = BN / WGN, MB = WM / 32, NB = WN / 32;
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be whole 32x32 blocks");
-  static constexpr int BK = BK_;
-  static_assert(BK == 32 || BK == 64, "slice depth");
-  static constexpr int KDIV = BK;  // K must be a multiple of the slice depth
+  static constexpr int BK = 64;
+  static constexpr int KDIV = BK;                 // K must be a multiple of the slice depth
+  static constexpr int NKK = BK / 16;             // MFMA sub-steps per slice
+  static_assert(NKK % 2 == 0, "register sets alternate per sub-step across slices");
   static constexpr int CPR = BK / 8;              // 16-byte chunks per row
   static constexpr int ROW_BYTES = BK * 2;
   static constexpr int RPW = 256 / ROW_BYTES;     // rows per 64-bank (256-byte) window
   static constexpr int RPI = 1024 / ROW_BYTES;    // rows per 1 KiB load instruction
-  static constexpr int ROWS = BM + BN;            // rows of one slice (A then B)
-  static constexpr int SLICE_BYTES = ROWS * ROW_BYTES;
-  static constexpr int GROUPS = ROWS / RPI;       // load instructions per slice
-  static_assert(ROWS % RPI == 0, "slice rows");
-  static constexpr int G_LO = GROUPS / NWAVES, G_REM = GROUPS % NWAVES;  // waves < G_REM do one more
-  static constexpr int LDS_ELEMS = STAGES * SLICE_BYTES / 2;
-  static_assert(STAGES >= 2, "ring depth");
+  static constexpr int SLICE_BYTES = (BM + BN) * ROW_BYTES;
+  static constexpr int A_LOADS = BM / RPI / NWAVES;  // load instructions per wave and slice
+  static constexpr int B_LOADS = BN / RPI / NWAVES;
+  static_assert(A_LOADS == 4 && B_LOADS == 4, "issue() is written for four load groups per operand");
+  static constexpr int LDS_ELEMS = 2 * SLICE_BYTES / 2;
 
   // Chunk c of slice row r lives in slot c ^ key(r): within one 256-byte window
   // the rows sit at distinct offsets, and key(r) differs for the CPR rows that
@@ -264,75 +279,119 @@ struct GemmDma {
   __device__ __forceinline__ static int wave_m(int wave) { return (wave / WGN) * WM; }
   __device__ __forceinline__ static int wave_n(int wave) { return (wave % WGN) * WN; }
 
-  // Issue this wave's loads of slice kt into ring slot (kt % STAGES).
-  __device__ __forceinline__ static void issue(const S* __restrict__ A, int64_t lda, int m0, int M,
-                                               const S* __restrict__ B, int64_t ldb, int n0, int N,
-                                               int kt, int nk, uint32_t lds0, int wave, int lane) {
-    const int kc = min(kt, nk - 1) * BK;  // past the end: reload the last slice (never read)
-    const uint32_t slot_base = lds0 + (uint32_t)((kt % STAGES) * SLICE_BYTES);
-    const int row_in = lane / CPR;        // RPI rows per instruction, CPR lanes per row
+  // Load instruction q of a wave covers the RPI slice rows starting at
+  // (wave + q * NWAVES) * RPI; A rows come first.  Rows at or beyond M (N) are
+  // clamped to the last row: they only feed accumulator rows (columns) that are
+  // never stored.
+  struct Loads {
+    const char* baseA;  // byte address of the tile's first A row (k = 0)
+    const char* baseB;
+    uint32_t offA[A_LOADS], offB[B_LOADS];  // per-lane byte offsets from the bases
+  };
+
+  __device__ __forceinline__ static void plan(Loads& L, const S* __restrict__ A, int64_t lda,
+                                              int m0, int M, const S* __restrict__ B, int64_t ldb,
+                                              int n0, int N, int wave, int lane) {
+    const int ma = min(m0, M - 1), nb = min(n0, N - 1);
+    L.baseA = (const char*)(A + (int64_t)ma * lda);
+    L.baseB = (const char*)(B + (int64_t)nb * ldb);
+    const int row_in = lane / CPR;
 #pragma unroll
-    for (int q = 0; q < G_LO + 1; ++q) {
-      if (q == G_LO && wave >= G_REM) break;
-      const int g = wave + q * NWAVES;
-      const int r = g * RPI + row_in;   // row within the slice
-      const int chunk = (lane % CPR) ^ key(r);
-      const S* src;
-      if (r < BM) {
-        src = A + (int64_t)min(m0 + r, M - 1) * lda + kc + 8 * chunk;
-      } else {
-        src = B + (int64_t)min(n0 + r - BM, N - 1) * ldb + kc + 8 * chunk;
-      }
-      lds_dma16(src, slot_base + (uint32_t)(g * 1024));
+    for (int q = 0; q < A_LOADS; ++q) {
+      const int r = (wave + q * NWAVES) * RPI + row_in;
+      const int c = (lane % CPR) ^ key(r);
+      L.offA[q] = (uint32_t)((min(m0 + r, M - 1) - ma) * lda * 2) + 16u * c;
+    }
+#pragma unroll
+    for (int q = 0; q < B_LOADS; ++q) {
+      const int r = (wave + (A_LOADS + q) * NWAVES) * RPI + row_in;  // >= BM
+      const int c = (lane % CPR) ^ key(r);
+      L.offB[q] = (uint32_t)((min(n0 + r - BM, N - 1) - nb) * ldb * 2) + 16u * c;
     }
   }
 
-  __device__ __forceinline__ static bf16x8_t frag(const S* slot, int row, int chunk) {
-    return *(const bf16x8_t*)(slot + row * BK + ((chunk ^ key(row)) << 3));
+  // Issue this wave's loads of slice kt into ring slot kt & 1.
+  __device__ __forceinline__ static void issue(const Loads& L, int kt, uint32_t lds0, int wave) {
+    const int64_t kb = (int64_t)kt * ROW_BYTES;
+    const uint32_t la = lds0 + (uint32_t)((kt & 1) * SLICE_BYTES + wave * 1024);
+    constexpr uint32_t STEP = NWAVES * 1024;  // LDS bytes between a wave's load groups
+    const uint32_t lb = la + A_LOADS * STEP;
+    lds_dma16x4(L.baseA + kb, L.offA[0], L.offA[1], L.offA[2], L.offA[3], la, la + STEP,
+                la + 2 * STEP, la + 3 * STEP);
+    lds_dma16x4(L.baseB + kb, L.offB[0], L.offB[1], L.offB[2], L.offB[3], lb, lb + STEP,
+                lb + 2 * STEP, lb + 3 * STEP);
   }
 
+  // Fragments of sub-step kk of the slice at `slot`: lane l takes row l % 32 of
+  // each 32-row block and k = 16 kk + 8 (l / 32) + 0..7, i.e. chunk 2 kk + l / 32.
+  __device__ __forceinline__ static void read(bf16x8_t (&a)[MB], bf16x8_t (&b)[NB], const S* slot,
+                                              int wm, int wn, int kk, int lane) {
+    const int chunk = 2 * kk + (lane >> 5);
+#pragma unroll
+    for (int i = 0; i < MB; ++i) {
+      const int row = wm + 32 * i + (lane & 31);
+      a[i] = *(const bf16x8_t*)(slot + row * BK + ((chunk ^ key(row)) << 3));
+    }
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      const int row = BM + wn + 32 * j + (lane & 31);
+      b[j] = *(const bf16x8_t*)(slot + row * BK + ((chunk ^ key(row)) << 3));
+    }
+  }
+
+  __device__ __forceinline__ static void mma(f32x16_t (&acc)[MB][NB], const bf16x8_t (&a)[MB],
+                                             const bf16x8_t (&b)[NB]) {
+#pragma unroll
+    for (int i = 0; i < MB; ++i)
+#pragma unroll
+      for (int j = 0; j < NB; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+  }
+
+  // acc += A[m0 : m0+BM, 0:K] B[n0 : n0+BN, 0:K]^T; requires m0 < M and n0 < N.
+  // LDS is free again for the caller when run() returns.
   __device__ __forceinline__ static void run(f32x16_t (&acc)[MB][NB], const S* __restrict__ A,
                                              int64_t lda, int m0, int M, const S* __restrict__ B,
                                              int64_t ldb, int n0, int N, int K, S* smem) {
-    // The wave index is made scalar so that the per-wave load counts below are
-    // taken on scalar branches: a vmcnt wait on a skipped path must not execute.
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave_m(wave), wn = wave_n(wave);
     const int nk = K / BK;
     if (nk <= 0) return;
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) S*)smem;
-#pragma unroll
-    for (int kt = 0; kt < STAGES - 1; ++kt) issue(A, lda, m0, M, B, ldb, n0, N, kt, nk, lds0, wave, lane);
+    Loads L;
+    plan(L, A, lda, m0, M, B, ldb, n0, N, wave, lane);
+    issue(L, 0, lds0, wave);
+    wait_vmcnt<0>();
+    __builtin_amdgcn_s_barrier();
+    if (nk > 1) issue(L, 1, lds0, wave);
+    bf16x8_t a[2][MB], b[2][NB];
+    read(a[0], b[0], smem, wm, wn, 0, lane);
     for (int kt = 0; kt < nk; ++kt) {
-      // this wave's loads of slice kt are done once only the STAGES-2 younger slices remain
-      if (wave < G_REM)
-        wait_vmcnt<(STAGES - 2) * (G_LO + 1)>();
-      else
-        wait_vmcnt<(STAGES - 2) * G_LO>();
-      __builtin_amdgcn_s_waitcnt(0xC07F);  // lgkmcnt(0): this wave's LDS reads of the last slice are done
-      __builtin_amdgcn_s_barrier();
-      const S* slot = smem + (kt % STAGES) * (SLICE_BYTES / 2);
+      const S* slot = smem + (kt & 1) * (SLICE_BYTES / 2);
 #pragma unroll
-      for (int kk = 0; kk < BK / 16; ++kk) {
-        // slot (kt-1) % STAGES is free since the barrier: refill it with slice kt + STAGES - 1
-        if (kk == ISSUE_AT) issue(A, lda, m0, M, B, ldb, n0, N, kt + STAGES - 1, nk, lds0, wave, lane);
-        bf16x8_t a[MB], b[NB];
-        const int chunk = 2 * kk + (lane >> 5);
-#pragma unroll
-        for (int i = 0; i < MB; ++i) a[i] = frag(slot, wm + 32 * i + (lane & 31), chunk);
-#pragma unroll
-        for (int j = 0; j < NB; ++j) b[j] = frag(slot, BM + wn + 32 * j + (lane & 31), chunk);
-#pragma unroll
-        for (int i = 0; i < MB; ++i)
-#pragma unroll
-          for (int j = 0; j < NB; ++j)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+      for (int kk = 0; kk < NKK; ++kk) {
+        const int cur = kk & 1;
+        if (kk + 1 < NKK) {
+          read(a[cur ^ 1], b[cur ^ 1], slot, wm, wn, kk + 1, lane);
+        } else {
+          // Taken on the last slice too (one spare barrier, fragments read from
+          // the idle slot and never used): no branch around the LDS reads, so
+          // the compiler's count of reads in flight stays exact and the MFMAs
+          // below wait only for the reads of this slice.
+          wait_vmcnt<0>();  // this wave's loads of slice kt+1
+          wait_lgkmcnt0();  // this wave's reads of slice kt
+          __builtin_amdgcn_s_barrier();
+          if (kt + 2 < nk) issue(L, kt + 2, lds0, wave);
+          read(a[cur ^ 1], b[cur ^ 1], smem + ((kt + 1) & 1) * (SLICE_BYTES / 2), wm, wn, 0, lane);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+        mma(acc, a[cur], b[cur]);
+        __builtin_amdgcn_sched_barrier(0);
       }
     }
-    // drain: no load may still be writing LDS when the caller reuses it
-    wait_vmcnt<0>();
-    __builtin_amdgcn_s_waitcnt(0xC07F);
+    // no wave may still be reading the ring when the caller reuses LDS
+    wait_lgkmcnt0();
     __builtin_amdgcn_s_barrier();
   }
 };

@@ -61,6 +61,13 @@ def test_workspace_size_independent_of_V():
     assert 0 < bwd <= 4 * (100 << 20) * eb + T * d * eb + d * 32768 * eb + 8192
 
 
+def test_largest_accepted_shapes():
+    fwd, bwd = vp.vp_ce_workspace_size(_prob(T=(1 << 23) - 256))
+    assert fwd > 0 and bwd > 0
+    fwd, bwd = vp.vp_ce_workspace_size(_prob(T=16, d=1 << 22))
+    assert fwd > 0 and bwd > 0
+
+
 def test_workspace_respects_strip_budget():
     T, d = 4096, 2880
     _, small = vp.vp_ce_workspace_size(_prob(T=T, d=d, strip_elems=1 << 20))
@@ -76,6 +83,8 @@ def test_workspace_respects_strip_budget():
     (dict(T=-1), vp.VP_ERR_SHAPE),
     (dict(d=0), vp.VP_ERR_SHAPE),
     (dict(d=12), vp.VP_ERR_SHAPE),
+    (dict(T=(1 << 23) - 255), vp.VP_ERR_SHAPE),
+    (dict(d=(1 << 22) + 8), vp.VP_ERR_SHAPE),
     (dict(shard_rows=[]), vp.VP_ERR_SHAPE),
     (dict(shard_rows=[1] * 65), vp.VP_ERR_SHAPE),
     (dict(shard_rows=[0, 0]), vp.VP_ERR_SHAPE),
