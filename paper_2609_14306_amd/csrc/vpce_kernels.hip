@@ -204,13 +204,16 @@ struct Gemm {
 // k = 16 kk .. 16 kk + 15 of the slice):
 //   sub-steps 0..2: read the fragments of sub-step kk+1 into the spare register
 //                   set, then issue the MFMAs of sub-step kk;
-//   sub-step 3:     wait for this wave's loads of slice kt+1, barrier, issue the
-//                   loads of slice kt+2 into slot kt & 1 (every wave finished
-//                   reading slice kt before the barrier), read the fragments of
-//                   slice kt+1 sub-step 0, then issue the MFMAs of sub-step 3.
+//   sub-step 3:     wait for this wave's loads of slice kt+1, barrier, read the
+//                   fragments of slice kt+1 sub-step 0, issue the MFMAs of
+//                   sub-step 3, then the loads of operand A of slice kt+2 into
+//                   slot kt & 1 (every wave finished reading slice kt before the
+//                   barrier); the loads of operand B of slice kt+2 follow the
+//                   MFMAs of sub-step 0 of slice kt+1.
 // The MFMAs never wait on an LDS read issued in the same sub-step, the only
 // barrier of a slice sits where every wave still holds a sub-step of MFMAs in
-// registers, and each slice's loads have a whole slice of MFMAs to land.
+// registers, each slice's loads have three or four sub-steps of MFMAs to land,
+// and a wave stalled on issuing loads has MFMAs queued ahead of it.
 //
 // The loads are issued from inline assembly with a scalar base (the tile's
 // first row at the slice's k offset) and a 32-bit per-lane byte offset, so that
@@ -253,7 +256,10 @@ struct GemmDma {
   using S = uint16_t;
   static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
   static constexpr int NT = 64 * WGM * WGN, NWAVES = WGM * WGN;
-  static constexpr int OCC = 512 / NT;  // two wavefronts per SIMD in total
+  // One workgroup per CU (the ring takes 128 KiB of LDS): 512 threads run two
+  // wavefronts per SIMD with 256 registers each, 256 threads one wavefront per
+  // SIMD with 512 (256 of them accumulation registers).
+  static constexpr int OCC = 1;
   static constexpr int WM = BM / WGM, WN = BN / WGN, MB = WM / 32, NB = WN / 32;
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be whole 32x32 blocks");
   static constexpr int BK = 64;
@@ -267,7 +273,7 @@ struct GemmDma {
   static constexpr int SLICE_BYTES = (BM + BN) * ROW_BYTES;
   static constexpr int A_LOADS = BM / RPI / NWAVES;  // load instructions per wave and slice
   static constexpr int B_LOADS = BN / RPI / NWAVES;
-  static_assert(A_LOADS == 4 && B_LOADS == 4, "issue() is written for four load groups per operand");
+  static_assert(A_LOADS % 4 == 0 && B_LOADS % 4 == 0, "loads are issued in blocks of four");
   static constexpr int LDS_ELEMS = 2 * SLICE_BYTES / 2;
 
   // Chunk c of slice row r lives in slot c ^ key(r): within one 256-byte window
@@ -310,16 +316,22 @@ struct GemmDma {
     }
   }
 
-  // Issue this wave's loads of slice kt into ring slot kt & 1.
+  // Issue this wave's loads of one operand of slice kt into ring slot kt & 1: load
+  // q of operand A fills the 1 KiB at (wave + q * NWAVES) KiB of the slot, load q
+  // of operand B the 1 KiB at (wave + (A_LOADS + q) * NWAVES) KiB.
+  template <int OP>
   __device__ __forceinline__ static void issue(const Loads& L, int kt, uint32_t lds0, int wave) {
     const int64_t kb = (int64_t)kt * ROW_BYTES;
-    const uint32_t la = lds0 + (uint32_t)((kt & 1) * SLICE_BYTES + wave * 1024);
-    constexpr uint32_t STEP = NWAVES * 1024;  // LDS bytes between a wave's load groups
-    const uint32_t lb = la + A_LOADS * STEP;
-    lds_dma16x4(L.baseA + kb, L.offA[0], L.offA[1], L.offA[2], L.offA[3], la, la + STEP,
-                la + 2 * STEP, la + 3 * STEP);
-    lds_dma16x4(L.baseB + kb, L.offB[0], L.offB[1], L.offB[2], L.offB[3], lb, lb + STEP,
-                lb + 2 * STEP, lb + 3 * STEP);
+    constexpr uint32_t STEP = NWAVES * 1024;
+    constexpr int NL = OP == 0 ? A_LOADS : B_LOADS;
+    const char* base = (OP == 0 ? L.baseA : L.baseB) + kb;
+    const uint32_t* off = OP == 0 ? L.offA : L.offB;
+    const uint32_t l = lds0 + (uint32_t)((kt & 1) * SLICE_BYTES + wave * 1024) +
+                       (OP == 0 ? 0u : A_LOADS * STEP);
+#pragma unroll
+    for (int q = 0; q < NL; q += 4)
+      lds_dma16x4(base, off[q], off[q + 1], off[q + 2], off[q + 3], l + q * STEP,
+                  l + (q + 1) * STEP, l + (q + 2) * STEP, l + (q + 3) * STEP);
   }
 
   // Fragments of sub-step kk of the slice at `slot`: lane l takes row l % 32 of
@@ -361,10 +373,14 @@ struct GemmDma {
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) S*)smem;
     Loads L;
     plan(L, A, lda, m0, M, B, ldb, n0, N, wave, lane);
-    issue(L, 0, lds0, wave);
+    issue<0>(L, 0, lds0, wave);
+    issue<1>(L, 0, lds0, wave);
     wait_vmcnt<0>();
     __builtin_amdgcn_s_barrier();
-    if (nk > 1) issue(L, 1, lds0, wave);
+    if (nk > 1) {
+      issue<0>(L, 1, lds0, wave);
+      issue<1>(L, 1, lds0, wave);
+    }
     bf16x8_t a[2][MB], b[2][NB];
     read(a[0], b[0], smem, wm, wn, 0, lane);
     for (int kt = 0; kt < nk; ++kt) {
@@ -382,11 +398,16 @@ struct GemmDma {
           wait_vmcnt<0>();  // this wave's loads of slice kt+1
           wait_lgkmcnt0();  // this wave's reads of slice kt
           __builtin_amdgcn_s_barrier();
-          if (kt + 2 < nk) issue(L, kt + 2, lds0, wave);
           read(a[cur ^ 1], b[cur ^ 1], smem + ((kt + 1) & 1) * (SLICE_BYTES / 2), wm, wn, 0, lane);
         }
         __builtin_amdgcn_sched_barrier(0);
         mma(acc, a[cur], b[cur]);
+        __builtin_amdgcn_sched_barrier(0);
+        // The loads of slice kt+2 go out in two halves behind MFMAs already issued:
+        // operand A after the last sub-step of slice kt, operand B after the first
+        // sub-step of slice kt+1 (slice 1 came whole from the prologue).
+        if (kk == NKK - 1 && kt + 2 < nk) issue<0>(L, kt + 2, lds0, wave);
+        if (kk == 0 && kt >= 1 && kt + 1 < nk) issue<1>(L, kt + 1, lds0, wave);
         __builtin_amdgcn_sched_barrier(0);
       }
     }
@@ -766,7 +787,10 @@ template <> struct Cfg<Bf16> {
   // 512-thread workgroups (two wavefronts per SIMD), 256 x 256 tiles, 128 x 64 per
   // wave, for every contraction (d = 2880 pads the dH / dW column tiles to 3072:
   // measured faster inside the backward stage launch than 256 x 192 tiles with
-  // 64 x 96 per wave, whose fragment reads per MFMA are higher).
+  // 64 x 96 per wave, whose fragment reads per MFMA are higher).  One wavefront
+  // per SIMD with 128 x 128 per wave reads a third less LDS per MFMA but measured
+  // 17% slower: a lone wave's load-issue stalls and barrier waits idle the MFMA
+  // pipe.
   using Logits = GemmDma<256, 256, 2, 4>;
   using MmA = GemmDma<256, 256, 2, 4>;
   using MmB = MmA;
