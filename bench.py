@@ -37,7 +37,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
-    ap.add_argument("--cpu-sample-rows", type=int, default=2048,
+    ap.add_argument("--cpu-sample-rows", type=int, default=4096,
                     help="token rows of the workload the CPU oracle is timed on")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--strip-elems", type=int, default=0)
@@ -142,6 +142,7 @@ def main():
     g = torch.full((T,), 1.0 / max(n_valid, 1), dtype=torch.float32, device=dev)
     prob = vp.problem_for(H, Ws, inp.ignore_index, inp.order, 0, args.strip_elems)
     fwd_b, bwd_b = vp.vp_ce_workspace_size(prob)
+    plan = vp.vp_ce_plan_info(prob)
     ws = torch.empty(max(fwd_b, bwd_b), dtype=torch.uint8, device=dev)
     loss = torch.empty(T, dtype=torch.float32, device=dev)
     lse = torch.empty(T, dtype=torch.float32, device=dev)
@@ -212,15 +213,21 @@ def main():
                             "allocated_during_steps": extra_alloc / 2**20,
                             "peak_over_resident": (max(fwd_b, bwd_b) + extra_alloc) / 2**20},
         # The dominant kernel by time: the backward stage kernel (recompute + residual,
-        # dH and dW tiles), launched once per strip plus once; achieved = 6TVd over the
-        # backward call's event time (which also holds ~1% of transposes), i.e. the
-        # average flops per launch over the average launch duration.
+        # dH and dW tiles), launched once per strip plus once.  Its average launch
+        # carries 6TVd / launches flops; its average duration is taken as the backward
+        # call's event time over the launch count (the call also holds the H and W
+        # transposes, about 1% of it, so achieved is slightly understated).
         "roofline": {"kernel": "bwd_stage_kernel (logits recompute + residual + dH + dW MFMA tiles)",
                      "bound": "mfma", "achieved": bwd_tflops, "peak": peak, "unit": "TFLOP/s",
-                     "frac": bwd_tflops / peak, "traffic": bwd_traffic},
+                     "frac": bwd_tflops / peak, "traffic": bwd_traffic,
+                     "launches_per_step": plan["stage_launches"],
+                     "flops_per_launch": 6.0 * T * V * d / max(plan["stage_launches"], 1),
+                     "avg_launch_ms": bwd_avg / max(plan["stage_launches"], 1),
+                     "strip": {"Tc": plan["Tc"], "Vc": plan["Vc"], "strips": plan["strips"]}},
         "roofline_fwd": {"kernel": "fwd_kernel (fused logits tiles + online LSE fold)",
                          "bound": "mfma", "achieved": fwd_tflops, "peak": peak, "unit": "TFLOP/s",
-                         "frac": fwd_tflops / peak, "traffic": fwd_traffic},
+                         "frac": fwd_tflops / peak, "traffic": fwd_traffic, "launches_per_step": 1,
+                         "flops_per_launch": 2.0 * T * V * d, "avg_launch_ms": fwd_avg},
         "bad_targets": bad,
         "input_gen_s": t_gen,
     }

@@ -123,6 +123,19 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
                          float* dH, float* const* dW_shards, void* ws, size_t ws_bytes,
                          void* stream);
 
+/* How vp_ce_backward cuts a problem (host only, needs no device): the residual
+ * strip is Tc tokens by at most Vc vocabulary rows; `strips` strips cover the
+ * T x V residual (each shard cut into balanced vocabulary chunks, each chunk
+ * meeting every token chunk), and the backward makes stage_launches = strips + 1
+ * launches of its fused recompute / residual / dH / dW kernel (0 when T == 0). */
+typedef struct {
+  int64_t Tc;
+  int64_t Vc;
+  int64_t strips;
+  int64_t stage_launches;
+} vp_plan_info;
+vp_status vp_ce_plan_info(const vp_problem* prob, vp_plan_info* info);
+
 /* Reads the count of out-of-range targets that the last forward or backward on
  * this workspace found (synchronises `stream`).  Returns VP_ERR_TARGET if it is
  * non-zero.  *bad_targets may be NULL. */

@@ -25,14 +25,19 @@ VP_F32, VP_BF16 = 0, 1
 VP_ACCUMULATE_DW = 1
 VP_MAX_SHARDS = 64
 
-EXPORTED = ("vp_ce_workspace_size", "vp_ce_forward", "vp_ce_backward", "vp_ce_check",
-            "vp_status_str", "vp_abi_version")
+EXPORTED = ("vp_ce_workspace_size", "vp_ce_forward", "vp_ce_backward", "vp_ce_plan_info",
+            "vp_ce_check", "vp_status_str", "vp_abi_version")
 
 
 class VpError(RuntimeError):
     def __init__(self, status: int, what: str):
         super().__init__(f"{what}: {vp_status_str(status)} (status {status})")
         self.status = status
+
+
+class vp_plan_info(ctypes.Structure):
+    _fields_ = [("Tc", ctypes.c_int64), ("Vc", ctypes.c_int64), ("strips", ctypes.c_int64),
+                ("stage_launches", ctypes.c_int64)]
 
 
 class vp_problem(ctypes.Structure):
@@ -75,6 +80,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vp_ce_backward.restype = ctypes.c_int
     lib.vp_ce_backward.argtypes = [vp, vptr, P(vptr), vptr, vptr, vptr, vptr, P(vptr), vptr,
                                    ctypes.c_size_t, vptr]
+    lib.vp_ce_plan_info.restype = ctypes.c_int
+    lib.vp_ce_plan_info.argtypes = [vp, P(vp_plan_info)]
     lib.vp_ce_check.restype = ctypes.c_int
     lib.vp_ce_check.argtypes = [vptr, vptr, P(ctypes.c_int64)]
     _lib = lib
@@ -135,6 +142,14 @@ def vp_ce_workspace_size(prob: Problem) -> Tuple[int, int]:
     _check(load_library().vp_ce_workspace_size(ctypes.byref(prob.c), ctypes.byref(f), ctypes.byref(b)),
            "vp_ce_workspace_size")
     return int(f.value), int(b.value)
+
+
+def vp_ce_plan_info(prob: Problem) -> dict:
+    """The backward's strip plan: Tc, Vc, strips and stage_launches (host only)."""
+    info = vp_plan_info()
+    _check(load_library().vp_ce_plan_info(ctypes.byref(prob.c), ctypes.byref(info)), "vp_ce_plan_info")
+    return {"Tc": int(info.Tc), "Vc": int(info.Vc), "strips": int(info.strips),
+            "stage_launches": int(info.stage_launches)}
 
 
 def vp_ce_forward(prob: Problem, H, W_shards, targets, loss, lse, ws, stream=None) -> None:

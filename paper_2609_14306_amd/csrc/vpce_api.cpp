@@ -231,6 +231,48 @@ vp_status vp_ce_forward(const vp_problem* prob, const void* H, const void* const
   return VP_OK;
 }
 
+// The strips of a backward call in visiting order: shards in `order`, each cut
+// into balanced, tile-aligned vocabulary chunks (never above Vc), each chunk
+// meeting every token chunk.
+struct Chunk {
+  int q;
+  int64_t v0, M, t0, N;
+  bool new_vchunk, first_vchunk;
+};
+
+std::vector<Chunk> strip_chunks(const vp_problem* prob, const StripPlan& plan) {
+  const vpce::TileShape ts = vpce::tile_shape(prob->dtype);
+  std::vector<Chunk> chunks;
+  bool first = true;
+  for (int i = 0; i < prob->P; ++i) {
+    const int q = prob->order ? prob->order[i] : i;
+    const int64_t Vq = prob->shard_rows[q];
+    if (Vq == 0) continue;
+    const int64_t vc =
+        std::min<int64_t>(plan.Vc, round_up(ceil_div(Vq, ceil_div(Vq, plan.Vc)), ts.grad_bm));
+    for (int64_t v0 = 0; v0 < Vq; v0 += vc) {
+      for (int64_t t0 = 0; t0 < prob->T; t0 += plan.Tc)
+        chunks.push_back({q, v0, std::min<int64_t>(vc, Vq - v0), t0,
+                          std::min<int64_t>(plan.Tc, prob->T - t0), t0 == 0, first});
+      first = false;
+    }
+  }
+  return chunks;
+}
+
+vp_status vp_ce_plan_info(const vp_problem* prob, vp_plan_info* info) {
+  const vp_status st = validate(prob, nullptr);
+  if (st != VP_OK) return st;
+  if (!info) return VP_ERR_NULL;
+  const StripPlan plan = strip_plan(prob);
+  const int64_t n = prob->T > 0 ? (int64_t)strip_chunks(prob, plan).size() : 0;
+  info->Tc = plan.Tc;
+  info->Vc = plan.Vc;
+  info->strips = n;
+  info->stage_launches = n > 0 ? n + 1 : 0;
+  return VP_OK;
+}
+
 vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* const* W_shards,
                          const int64_t* targets, const float* lse, const float* grad_loss,
                          float* dH, float* const* dW_shards, void* ws, size_t ws_bytes,
@@ -285,31 +327,7 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
     if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
   }
 
-  // The strips in visiting order: shards in `order`, each cut into balanced,
-  // tile-aligned vocabulary chunks (never above Vc), each chunk meeting every
-  // token chunk.
-  struct Chunk {
-    int q;
-    int64_t v0, M, t0, N;
-    bool new_vchunk, first_vchunk;
-  };
-  std::vector<Chunk> chunks;
-  {
-    bool first = true;
-    for (int i = 0; i < prob->P; ++i) {
-      const int q = prob->order ? prob->order[i] : i;
-      const int64_t Vq = prob->shard_rows[q];
-      if (Vq == 0) continue;
-      const int64_t vc = std::min<int64_t>(
-          plan.Vc, round_up(ceil_div(Vq, ceil_div(Vq, plan.Vc)), ts.grad_bm));
-      for (int64_t v0 = 0; v0 < Vq; v0 += vc) {
-        for (int64_t t0 = 0; t0 < T; t0 += plan.Tc)
-          chunks.push_back({q, v0, std::min<int64_t>(vc, Vq - v0), t0,
-                            std::min<int64_t>(plan.Tc, T - t0), t0 == 0, first});
-        first = false;
-      }
-    }
-  }
+  const std::vector<Chunk> chunks = strip_chunks(prob, plan);
   int64_t off[VP_MAX_SHARDS];
   int64_t acc = 0;
   for (int q = 0; q < prob->P; ++q) {

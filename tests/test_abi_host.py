@@ -68,6 +68,20 @@ def test_largest_accepted_shapes():
     assert fwd > 0 and bwd > 0
 
 
+def test_plan_info():
+    # long-context shape: 8192-token strips, shards of 25136 rows cut in two chunks
+    info = vp.vp_ce_plan_info(_prob(T=32768))
+    assert info["Tc"] == 8192 and info["Vc"] == 12800
+    assert info["strips"] == 8 * 2 * 4 and info["stage_launches"] == 65
+    assert vp.vp_ce_plan_info(_prob(T=0))["stage_launches"] == 0
+    one = vp.vp_ce_plan_info(_prob(T=1, shard_rows=[100, 0, 5]))
+    assert one["strips"] == 2 and one["stage_launches"] == 3
+    with pytest.raises(vp.VpError):
+        vp.vp_ce_plan_info(_prob(T=-1))
+    lib = vp.load_library()
+    assert lib.vp_ce_plan_info(ctypes.byref(_prob().c), None) == vp.VP_ERR_NULL
+
+
 def test_workspace_respects_strip_budget():
     T, d = 4096, 2880
     _, small = vp.vp_ce_workspace_size(_prob(T=T, d=d, strip_elems=1 << 20))
