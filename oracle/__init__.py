@@ -17,7 +17,9 @@ What it computes (Sec. 3.2 of the paper, and the appendix section on Ring-DTP):
   tokens), dH = G W and dW = G^T H, W being the vocabulary projection in
   [V, d] row layout;
 * the ring form of the forward: Algorithm 2's Fold applied shard by shard in any
-  visiting order, the running state (m, z, y) starting at (-inf, 0, 0).
+  visiting order, the running state (m, z, y) starting at (-inf, 0, 0); one
+  meeting (``fold_shard``) is what a move-activations hop carries the state
+  through, and ``fold_finalize`` turns the state into (loss, lse).
 
 Everything is float64.  Inputs arrive as the exact float64 widening of the bits
 the GPU path receives.  Every function here is pinned by a test in
@@ -28,6 +30,9 @@ from .ce import (  # noqa: F401
     backward_rows,
     concat_shards,
     dW_rows,
+    fold_finalize,
+    fold_init,
+    fold_shard,
     forward,
     forward_backward,
     forward_rows,

@@ -137,17 +137,50 @@ def forward_backward(H: np.ndarray, W_shards: Sequence[np.ndarray], targets: np.
             "max_abs_logit": max_abs}
 
 
+def fold_init(T: int):
+    """Algorithm 2's initial per-token state (m, z, y) = (-inf, 0, 0)."""
+    return np.full(T, -np.inf), np.zeros(T), np.zeros(T)
+
+
+def fold_shard(state, H: np.ndarray, W_q: np.ndarray, off_q: int, targets: np.ndarray):
+    """One meeting of Algorithm 2: fold the logit strip of one shard into the state.
+
+    The shard owns global ids [off_q, off_q + V_q).  With Y = H W_q^T (the strip of
+    this meeting), the online-softmax update of Sec. 3.2 gives
+    m' = max(m, max_v Y_v) and z' = e^{m - m'} z + sum_v e^{Y_v - m'}; the target
+    logit y is written by the one shard whose interval holds the target.  An empty
+    strip leaves the state unchanged (reading for the -inf - -inf case).
+    Returns a new state; the input is not modified.
+    """
+    m, z, y = (np.array(a, dtype=np.float64, copy=True) for a in state)
+    W_q = np.asarray(W_q, dtype=np.float64)
+    targets = np.asarray(targets, dtype=np.int64)
+    V_q = W_q.shape[0]
+    if V_q == 0:
+        return m, z, y
+    Y = np.asarray(H, dtype=np.float64) @ W_q.T
+    m_new = np.maximum(m, Y.max(axis=1))
+    z = np.exp(m - m_new) * z + np.exp(Y - m_new[:, None]).sum(axis=1)
+    own = (targets >= off_q) & (targets < off_q + V_q)
+    y[own] = Y[np.nonzero(own)[0], targets[own] - off_q]
+    return m_new, z, y
+
+
+def fold_finalize(state, targets: np.ndarray, V: int, ignore_index: int = -100):
+    """(loss, lse) from a state that has met every shard: lse = m + log z, loss = lse - y
+    (0 for ignored tokens, NaN for targets outside [0, V))."""
+    m, z, y = state
+    lse = m + np.log(z)
+    ignored, bad = _valid(np.asarray(targets, dtype=np.int64), V, ignore_index)
+    loss = np.where(ignored, 0.0, lse - y)
+    loss[bad] = np.nan
+    return loss, lse
+
+
 def ring_forward(H: np.ndarray, W_shards: Sequence[np.ndarray], targets: np.ndarray,
                  order: Optional[Sequence[int]] = None, ignore_index: int = -100):
-    """Algorithm 2's forward on one rank: fold each shard's logit strip in visiting order.
-
-    State per token is (m, z, y): running maximum, exponential sum relative to m,
-    and the target logit (written only by the one shard interval that holds the
-    target).  Initial state (-inf, 0, 0).  Fold rule (the online-softmax update of
-    Sec. 3.2): m' = max(m, max_v y_v), z' = e^{m - m'} z + sum_v e^{y_v - m'}.
-    An empty strip leaves the state unchanged (reading for the -inf - -inf case).
-    Output: loss = m + log z - y (0 for ignored tokens), lse = m + log z.
-    """
+    """Algorithm 2's forward on one rank: fold each shard's logit strip in visiting order
+    (fold_shard per meeting), then finalize.  Returns (loss, lse, final state)."""
     H = np.asarray(H, dtype=np.float64)
     targets = np.asarray(targets, dtype=np.int64)
     P = len(W_shards)
@@ -156,26 +189,11 @@ def ring_forward(H: np.ndarray, W_shards: Sequence[np.ndarray], targets: np.ndar
         raise ValueError("order must be a permutation of the shards")
     rows = [np.asarray(w).shape[0] for w in W_shards]
     offs = np.cumsum([0] + rows)
-    T = H.shape[0]
-    m = np.full(T, -np.inf)
-    z = np.zeros(T)
-    y = np.zeros(T)
+    state = fold_init(H.shape[0])
     for q in order:
-        if rows[q] == 0:
-            continue
-        Y = H @ np.asarray(W_shards[q], dtype=np.float64).T  # the strip of this meeting
-        m_new = np.maximum(m, Y.max(axis=1))
-        z = np.exp(m - m_new) * z + np.exp(Y - m_new[:, None]).sum(axis=1)
-        m = m_new
-        lo, hi = offs[q], offs[q + 1]
-        own = (targets >= lo) & (targets < hi)
-        y[own] = Y[np.nonzero(own)[0], targets[own] - lo]
-    lse = m + np.log(z)
-    V = int(offs[-1])
-    ignored, bad = _valid(targets, V, ignore_index)
-    loss = np.where(ignored, 0.0, lse - y)
-    loss[bad] = np.nan
-    return loss, lse, (m, z, y)
+        state = fold_shard(state, H, W_shards[q], int(offs[q]), targets)
+    loss, lse = fold_finalize(state, targets, int(offs[-1]), ignore_index)
+    return loss, lse, state
 
 
 def scalar_forward_backward(H, W, targets, grad_loss, ignore_index: int = -100):

@@ -183,6 +183,38 @@ def pin_fold_order_invariance(ce):
         np.testing.assert_allclose(m, Y.max(axis=1), rtol=0, atol=0)
 
 
+def pin_fold_state_passing(ce):
+    """A state carried from meeting to meeting (one move-activations hop per shard, a shard
+    cut in two at an arbitrary id, an empty shard) is, after any subset of meetings, the
+    closed form over exactly the ids met so far: m = max of their logits, z = sum of
+    e^{logit - m}, y = the target logit if the target was among them; after all of
+    them it finalizes to the dense definition."""
+    H, W, t, g, shards = _problem(8, T=11, d=5, V=23, rows=(6, 9, 0, 8), ignore=(4,))
+    loss, lse = ce.forward(H, W, t, IGN)
+    Y = H @ W.T
+    # meetings: (global id offset, rows); shard 1 is cut at id 6 + 4
+    meets = [(15, W[15:23]), (6, W[6:10]), (23, W[23:23]), (0, W[0:6]), (10, W[10:15])]
+    state = ce.fold_init(H.shape[0])
+    seen = np.zeros(W.shape[0], dtype=bool)
+    for off, Wq in meets:
+        state = ce.fold_shard(state, H, Wq, off, t)
+        seen[off:off + Wq.shape[0]] = True
+        if not seen.any():
+            assert np.all(state[0] == -np.inf) and np.all(state[1] == 0.0)
+            continue
+        m_ref = Y[:, seen].max(axis=1)
+        z_ref = np.exp(Y[:, seen] - m_ref[:, None]).sum(axis=1)
+        np.testing.assert_allclose(state[0], m_ref, rtol=0, atol=0)
+        np.testing.assert_allclose(state[1], z_ref, rtol=1e-13)
+        met = (t >= 0) & (t < W.shape[0]) & (t != IGN)
+        met[met] = seen[t[met]]
+        np.testing.assert_allclose(state[2][met], Y[np.nonzero(met)[0], t[met]], rtol=0, atol=0)
+        np.testing.assert_array_equal(state[2][~met], 0.0)
+    fl, flse = ce.fold_finalize(state, t, W.shape[0], IGN)
+    np.testing.assert_allclose(flse, lse, rtol=1e-12)
+    np.testing.assert_allclose(fl, loss, rtol=1e-12, atol=1e-13)
+
+
 def pin_finite_differences(ce):
     """Central differences of sum_t g_t loss_t in float64 match the analytic dH and dW."""
     H, W, t, g, _ = _problem(6, T=4, d=8, V=16, rows=(16,), ignore=(3,))
@@ -299,6 +331,7 @@ ALL_PINS = [
     pin_two_class_logistic,
     pin_shift_invariance,
     pin_fold_order_invariance,
+    pin_fold_state_passing,
     pin_finite_differences,
     pin_ignore_masking,
     pin_invariants,

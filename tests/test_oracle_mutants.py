@@ -61,36 +61,33 @@ def _fwd_target_off_by_one(Y, t, ign):
     return _orig_fwd(Y, t2, ign)
 
 
-def _make_ring(variant):
-    def ring_forward(H, W_shards, targets, order=None, ignore_index=-100):
-        H = np.asarray(H, dtype=np.float64)
+def _make_fold(variant):
+    def fold_shard(state, H, W_q, off_q, targets):
+        m, z, y = (np.array(a, dtype=np.float64, copy=True) for a in state)
+        W_q = np.asarray(W_q, dtype=np.float64)
         targets = np.asarray(targets, dtype=np.int64)
-        P = len(W_shards)
-        order = list(range(P)) if order is None else list(order)
-        rows = [np.asarray(w).shape[0] for w in W_shards]
-        offs = np.cumsum([0] + rows)
-        T = H.shape[0]
-        m = np.full(T, -np.inf); z = np.zeros(T); y = np.zeros(T)
-        for q in order:
-            if rows[q] == 0:
-                continue
-            Y = H @ np.asarray(W_shards[q], dtype=np.float64).T
-            m_new = np.maximum(m, Y.max(axis=1))
-            if variant == "no_rescale":
-                z = z + np.exp(Y - m_new[:, None]).sum(axis=1)
-            else:
-                z = np.exp(m - m_new) * z + np.exp(Y - m_new[:, None]).sum(axis=1)
-            m = m_new
-            lo, hi = offs[q], offs[q + 1]
-            if variant == "interval_open":
-                own = (targets > lo) & (targets < hi)
-            else:
-                own = (targets >= lo) & (targets < hi)
-            y[own] = Y[np.nonzero(own)[0], targets[own] - lo]
-        lse = m + np.log(z)
-        loss = np.where(targets == ignore_index, 0.0, lse - y)
-        return loss, lse, (m, z, y)
-    return ring_forward
+        if W_q.shape[0] == 0:
+            return m, z, y
+        Y = np.asarray(H, dtype=np.float64) @ W_q.T
+        m_new = np.maximum(m, Y.max(axis=1))
+        if variant == "no_rescale":
+            z = z + np.exp(Y - m_new[:, None]).sum(axis=1)
+        else:
+            z = np.exp(m - m_new) * z + np.exp(Y - m_new[:, None]).sum(axis=1)
+        lo, hi = off_q, off_q + W_q.shape[0]
+        if variant == "interval_open":
+            own = (targets > lo) & (targets < hi)
+        else:
+            own = (targets >= lo) & (targets < hi)
+        y[own] = Y[np.nonzero(own)[0], targets[own] - lo]
+        return m_new, z, y
+    return fold_shard
+
+
+def _finalize_target_added(state, targets, V, ignore_index=-100):
+    m, z, y = state
+    lse = m + np.log(z)
+    return np.where(np.asarray(targets) == ignore_index, 0.0, lse + y), lse
 
 
 def _make_backward(variant):
@@ -129,8 +126,9 @@ MUTANTS = {
     "lse_is_max_only": {"_forward_chunk": _fwd_max_only},
     "loss_sign_of_target_logit": {"_forward_chunk": _fwd_loss_sign},
     "target_gather_off_by_one": {"_forward_chunk": _fwd_target_off_by_one},
-    "fold_without_rescale": {"ring_forward": _make_ring("no_rescale")},
-    "fold_interval_excludes_first_id": {"ring_forward": _make_ring("interval_open")},
+    "fold_without_rescale": {"fold_shard": _make_fold("no_rescale")},
+    "fold_interval_excludes_first_id": {"fold_shard": _make_fold("interval_open")},
+    "fold_finalize_adds_target_logit": {"fold_finalize": _finalize_target_added},
     "dW_token_rows_permuted": {"backward": _make_backward("dW_rows_reversed"),
                                "forward_backward": _fb_from(_make_backward("dW_rows_reversed"))},
     "dH_vocab_rows_permuted": {"backward": _make_backward("dH_vocab_reversed"),
