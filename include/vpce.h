@@ -56,7 +56,7 @@ typedef enum {
                              [1, 2^31 - 1], strip_elems out of [0, 2^30] */
   VP_ERR_DTYPE = 3,       /* dtype is not VP_F32 / VP_BF16 */
   VP_ERR_ORDER = 4,       /* order is not a permutation of 0..P-1 */
-  VP_ERR_ALIGN = 5,       /* a device pointer is not 16-byte aligned */
+  VP_ERR_ALIGN = 5,       /* a device pointer is not 16-byte aligned (4 for a fold state) */
   VP_ERR_WORKSPACE = 6,   /* workspace pointer NULL or smaller than the size the library asked for */
   VP_ERR_TARGET = 7,      /* (vp_ce_check) some target was outside [0, V) and not ignore_index */
   VP_ERR_HIP = 8,         /* a HIP runtime call or a kernel launch failed */
@@ -122,6 +122,52 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
                          const int64_t* targets, const float* lse, const float* grad_loss,
                          float* dH, float* const* dW_shards, void* ws, size_t ws_bytes,
                          void* stream);
+
+/* Per-shard fold: one meeting of Algorithm 2 at a time, for a per-token state
+ * that travels with the activations (move-activations: the hidden states, the
+ * targets and the state visit the ranks that hold the vocabulary shards, and a
+ * final hop returns the state to its owner, Sec. 3.2 and Algorithm 2).
+ *
+ * State: device float32 [3 * T], three planes of T values:
+ *   m[t]  = state[t]          running maximum logit over the vocabulary ids folded so
+ *                             far (natural units), -inf before the first shard;
+ *   s[t]  = state[T + t]      sum over those ids of exp(y_tv - m[t]);
+ *   y[t]  = state[2T + t]     the target logit h_t . w_{targets[t]} once the shard
+ *                             owning targets[t] has been folded, 0 before.
+ * The planes are plain numbers in host byte order: the state is serialised by
+ * copying its 12 T bytes, on any device or the host, and folding may resume
+ * from such a copy on another device.  Folding is order-free up to rounding
+ * (the online-softmax update is associative and commutative). */
+
+/* state <- (-inf, 0, 0) for every token.  state: device float32 [3 * T], 4-byte
+ * aligned; T in [0, 2^23 - 256] (VP_ERR_SHAPE otherwise). */
+vp_status vp_ce_state_init(float* state, int64_t T, void* stream);
+
+/* Folds one vocabulary shard into the state (the online-softmax update of Sec. 3.2):
+ *   m' = max(m, max_v y_tv),  s' = s e^(m - m') + sum_v e^(y_tv - m'),
+ *   y' = y_{t, targets[t]} where id_offset <= targets[t] < id_offset + V_q, else y.
+ * shard: a vp_problem with P == 1 whose shard_rows[0] = V_q are the shard's rows
+ * (T, d, dtype as for vp_ce_forward; order NULL or {0}; ignore_index, flags and
+ * strip_elems unused); id_offset: the global vocabulary id of the shard's first
+ * row (id_offset + V_q <= 2^31 - 1).  H: device [T, d]; W_shard: device [V_q, d]
+ * (NULL allowed when V_q == 0); targets: device int64 [T] of global ids; state as
+ * above, updated in place.  ws: the forward workspace of `shard`
+ * (vp_ce_workspace_size(shard, &fwd, NULL); it depends on T only, so for V_q == 0,
+ * which vp_ce_workspace_size rejects, any problem with the same T gives it),
+ * 16-byte aligned.  V_q == 0 or T == 0 leaves the state unchanged. */
+vp_status vp_ce_fold_shard(const vp_problem* shard, int64_t id_offset, const void* H,
+                           const void* W_shard, const int64_t* targets, float* state, void* ws,
+                           size_t ws_bytes, void* stream);
+
+/* From a state that has met every shard of the vocabulary described by `prob`
+ * (V = sum of its shard_rows; T and ignore_index as for vp_ce_forward):
+ *   lse[t]  = m[t] + log s[t],
+ *   loss[t] = lse[t] - y[t], 0 if targets[t] == ignore_index, NaN if targets[t] is
+ *             outside [0, V) (counted in ws for vp_ce_check).
+ * The state is only read.  ws: at least 256 bytes (the forward workspace of any
+ * problem is enough), 16-byte aligned. */
+vp_status vp_ce_fold_finalize(const vp_problem* prob, const int64_t* targets, const float* state,
+                              float* loss, float* lse, void* ws, size_t ws_bytes, void* stream);
 
 /* How vp_ce_backward cuts a problem (host only, needs no device): the residual
  * strip is Tc tokens by at most Vc vocabulary rows; `strips` strips cover the

@@ -25,8 +25,9 @@ VP_F32, VP_BF16 = 0, 1
 VP_ACCUMULATE_DW = 1
 VP_MAX_SHARDS = 64
 
-EXPORTED = ("vp_ce_workspace_size", "vp_ce_forward", "vp_ce_backward", "vp_ce_plan_info",
-            "vp_ce_check", "vp_status_str", "vp_abi_version")
+EXPORTED = ("vp_ce_workspace_size", "vp_ce_forward", "vp_ce_backward", "vp_ce_state_init",
+            "vp_ce_fold_shard", "vp_ce_fold_finalize", "vp_ce_plan_info", "vp_ce_check",
+            "vp_status_str", "vp_abi_version")
 
 
 class VpError(RuntimeError):
@@ -80,6 +81,13 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vp_ce_backward.restype = ctypes.c_int
     lib.vp_ce_backward.argtypes = [vp, vptr, P(vptr), vptr, vptr, vptr, vptr, P(vptr), vptr,
                                    ctypes.c_size_t, vptr]
+    lib.vp_ce_state_init.restype = ctypes.c_int
+    lib.vp_ce_state_init.argtypes = [vptr, ctypes.c_int64, vptr]
+    lib.vp_ce_fold_shard.restype = ctypes.c_int
+    lib.vp_ce_fold_shard.argtypes = [vp, ctypes.c_int64, vptr, vptr, vptr, vptr, vptr, ctypes.c_size_t,
+                                     vptr]
+    lib.vp_ce_fold_finalize.restype = ctypes.c_int
+    lib.vp_ce_fold_finalize.argtypes = [vp, vptr, vptr, vptr, vptr, vptr, ctypes.c_size_t, vptr]
     lib.vp_ce_plan_info.restype = ctypes.c_int
     lib.vp_ce_plan_info.argtypes = [vp, P(vp_plan_info)]
     lib.vp_ce_check.restype = ctypes.c_int
@@ -144,6 +152,26 @@ def vp_ce_workspace_size(prob: Problem) -> Tuple[int, int]:
     return int(f.value), int(b.value)
 
 
+def vp_ce_state_init(state, T: int, stream=None) -> None:
+    _check(load_library().vp_ce_state_init(_ptr(state), int(T), _stream(stream)), "vp_ce_state_init")
+
+
+def vp_ce_fold_shard(shard: Problem, id_offset: int, H, W_shard, targets, state, ws,
+                     stream=None) -> None:
+    st = load_library().vp_ce_fold_shard(ctypes.byref(shard.c), int(id_offset), _ptr(H),
+                                         _ptr(W_shard) if W_shard is not None and W_shard.numel() else None,
+                                         _ptr(targets), _ptr(state), _ptr(ws),
+                                         ws.numel() * ws.element_size(), _stream(stream))
+    _check(st, "vp_ce_fold_shard")
+
+
+def vp_ce_fold_finalize(prob: Problem, targets, state, loss, lse, ws, stream=None) -> None:
+    st = load_library().vp_ce_fold_finalize(ctypes.byref(prob.c), _ptr(targets), _ptr(state), _ptr(loss),
+                                            _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
+                                            _stream(stream))
+    _check(st, "vp_ce_fold_finalize")
+
+
 def vp_ce_plan_info(prob: Problem) -> dict:
     """The backward's strip plan: Tc, Vc, strips and stage_launches (host only)."""
     info = vp_plan_info()
@@ -204,6 +232,41 @@ def forward(H, W_shards: List, targets, ignore_index: int = -100, order=None, ws
     loss = torch.empty(prob.T, dtype=torch.float32, device=H.device)
     lse = torch.empty(prob.T, dtype=torch.float32, device=H.device)
     vp_ce_forward(prob, H, W_shards, targets, loss, lse, ws)
+    return loss, lse
+
+
+def new_state(T: int, device):
+    """A fold state float32 [3 * T] set to (-inf, 0, 0) on `device`."""
+    import torch
+    state = torch.empty(3 * int(T), dtype=torch.float32, device=device)
+    vp_ce_state_init(state, T)
+    return state
+
+
+def fold_shard(H, W_shard, id_offset: int, targets, state, ws=None) -> None:
+    """Folds the shard W_shard [V_q, d] owning global ids [id_offset, id_offset + V_q) into
+    `state` (one meeting of Algorithm 2, in place)."""
+    import torch
+    if W_shard.shape[0] == 0:
+        return  # an empty strip leaves the state unchanged
+    shard = problem_for(H, [W_shard])
+    fwd_b, _ = vp_ce_workspace_size(shard)
+    if ws is None or ws.numel() * ws.element_size() < fwd_b:
+        ws = torch.empty(fwd_b, dtype=torch.uint8, device=H.device)
+    vp_ce_fold_shard(shard, id_offset, H, W_shard, targets, state, ws)
+
+
+def fold_finalize(targets, state, shard_rows: Sequence[int], ignore_index: int = -100, ws=None):
+    """(loss, lse) float32 [T] from a state that has met every shard of the vocabulary
+    whose shards have `shard_rows` rows."""
+    import torch
+    T = int(targets.shape[0])
+    prob = Problem(T, 8, list(shard_rows), VP_BF16, None, ignore_index)
+    if ws is None:
+        ws = torch.empty(256, dtype=torch.uint8, device=targets.device)
+    loss = torch.empty(T, dtype=torch.float32, device=targets.device)
+    lse = torch.empty(T, dtype=torch.float32, device=targets.device)
+    vp_ce_fold_finalize(prob, targets, state, loss, lse, ws)
     return loss, lse
 
 

@@ -29,7 +29,7 @@ size_t elem_bytes(int dtype) { return dtype == VP_BF16 ? 2 : 4; }
 constexpr int64_t kMaxT = (1ll << 23) - 256;
 constexpr int64_t kMaxD = 1ll << 22;
 
-vp_status validate(const vp_problem* p, int64_t* V_out) {
+vp_status validate(const vp_problem* p, int64_t* V_out, bool allow_empty_vocab = false) {
   if (!p) return VP_ERR_NULL;
   if (p->dtype != VP_F32 && p->dtype != VP_BF16) return VP_ERR_DTYPE;
   // The bf16 GEMM tiles address a 256-row operand tile with 32-bit byte offsets
@@ -45,7 +45,7 @@ vp_status validate(const vp_problem* p, int64_t* V_out) {
     if (p->shard_rows[i] < 0 || p->shard_rows[i] > (1ll << 30)) return VP_ERR_SHAPE;
     V += p->shard_rows[i];
   }
-  if (V < 1 || V > (1ll << 31) - 1) return VP_ERR_SHAPE;
+  if (V < (allow_empty_vocab ? 0 : 1) || V > (1ll << 31) - 1) return VP_ERR_SHAPE;
   if (p->order) {
     bool seen[VP_MAX_SHARDS] = {false};
     for (int i = 0; i < p->P; ++i) {
@@ -229,6 +229,94 @@ vp_status vp_ce_forward(const vp_problem* prob, const void* H, const void* const
   c.bad_counter = counter;
   if (!vpce::run_comb(c, s)) return VP_ERR_HIP;
   return VP_OK;
+}
+
+vp_status vp_ce_state_init(float* state, int64_t T, void* stream) {
+  if (T < 0 || T > kMaxT) return VP_ERR_SHAPE;
+  if (T == 0) return VP_OK;
+  if (!state) return VP_ERR_NULL;
+  if (((uintptr_t)state & 3u) != 0) return VP_ERR_ALIGN;
+  return vpce::run_state_init(state, T, (hipStream_t)stream) ? VP_OK : VP_ERR_HIP;
+}
+
+vp_status vp_ce_fold_shard(const vp_problem* shard, int64_t id_offset, const void* H,
+                           const void* W_shard, const int64_t* targets, float* state, void* ws,
+                           size_t ws_bytes, void* stream) {
+  int64_t Vq = 0;
+  vp_status st = validate(shard, &Vq, /*allow_empty_vocab=*/true);
+  if (st != VP_OK) return st;
+  if (shard->P != 1) return VP_ERR_SHAPE;
+  if (id_offset < 0 || id_offset > (1ll << 31) - 1 - Vq) return VP_ERR_SHAPE;
+  if (!ws) return VP_ERR_WORKSPACE;
+  if (ws_bytes < fwd_ws_bytes(shard)) return VP_ERR_WORKSPACE;
+  if (misaligned(ws)) return VP_ERR_ALIGN;
+  const int64_t T = shard->T;
+  if (T == 0 || Vq == 0) return VP_OK;  // an empty strip leaves the state unchanged
+  if (!H || !W_shard || !targets || !state) return VP_ERR_NULL;
+  if (misaligned(H) || misaligned(W_shard)) return VP_ERR_ALIGN;
+  if (((uintptr_t)state & 3u) != 0) return VP_ERR_ALIGN;
+  hipStream_t s = (hipStream_t)stream;
+
+  const vpce::TileShape ts = vpce::tile_shape(shard->dtype);
+  const int32_t tiles = (int32_t)ceil_div(Vq, ts.fwd_bm);
+  const int S = std::min(splits_for(shard), (int)tiles);
+  char* base = (char*)ws + kHeaderBytes;
+  vpce::FwdArgs a;
+  memset(&a, 0, sizeof(a));
+  a.st.P = 1;
+  a.st.w[0] = W_shard;
+  a.st.off[0] = id_offset;
+  a.st.rows[0] = (int32_t)Vq;
+  a.st.tile0[0] = 0;
+  for (int i = 1; i <= VP_MAX_SHARDS; ++i) a.st.tile0[i] = tiles;
+  for (int i = 1; i < VP_MAX_SHARDS; ++i) a.st.off[i] = id_offset + Vq;
+  a.n_tiles = tiles;
+  a.H = H;
+  a.targets = targets;
+  a.T = T;
+  a.d = (int32_t)shard->d;
+  a.n_tok_blocks = (int32_t)ceil_div(T, ts.fwd_bn);
+  a.n_splits = S;
+  a.m_part = (float*)base;
+  a.s_part = (float*)(base + align256((size_t)S * T * 4));
+  a.y_tgt = state + 2 * T;  // written only for targets this shard owns
+  if (!vpce::run_fwd(shard->dtype, a, s)) return VP_ERR_HIP;
+
+  vpce::FoldArgs f;
+  f.m_part = a.m_part;
+  f.s_part = a.s_part;
+  f.T = T;
+  f.n_splits = S;
+  f.state = state;
+  return vpce::run_fold_merge(f, s) ? VP_OK : VP_ERR_HIP;
+}
+
+vp_status vp_ce_fold_finalize(const vp_problem* prob, const int64_t* targets, const float* state,
+                              float* loss, float* lse, void* ws, size_t ws_bytes, void* stream) {
+  int64_t V = 0;
+  vp_status st = validate(prob, &V);
+  if (st != VP_OK) return st;
+  if (!ws) return VP_ERR_WORKSPACE;
+  if (ws_bytes < kHeaderBytes) return VP_ERR_WORKSPACE;
+  if (misaligned(ws)) return VP_ERR_ALIGN;
+  const int64_t T = prob->T;
+  if (T > 0) {
+    if (!targets || !state || !loss || !lse) return VP_ERR_NULL;
+    if (((uintptr_t)state & 3u) != 0) return VP_ERR_ALIGN;
+  }
+  hipStream_t s = (hipStream_t)stream;
+  unsigned long long* counter = (unsigned long long*)ws;
+  if (!vpce::run_ws_init(counter, s)) return VP_ERR_HIP;
+  vpce::FinArgs f;
+  f.state = state;
+  f.targets = targets;
+  f.T = T;
+  f.V = V;
+  f.ignore_index = prob->ignore_index;
+  f.loss = loss;
+  f.lse = lse;
+  f.bad_counter = counter;
+  return vpce::run_fold_finalize(f, s) ? VP_OK : VP_ERR_HIP;
 }
 
 // The strips of a backward call in visiting order: shards in `order`, each cut

@@ -42,6 +42,26 @@ struct CombArgs {
   unsigned long long* bad_counter;
 };
 
+// Per-token fold state of Algorithm 2 as the ABI exposes it: float32 [3][T],
+// planes m (running maximum logit, natural units), s (sum of e^(y - m) over the
+// ids folded so far) and y (the target logit once its shard has been folded).
+struct FoldArgs {
+  const float* m_part;  // [n_splits][T], base-2 domain (max of y log2 e)
+  const float* s_part;  // [n_splits][T]
+  int64_t T;
+  int32_t n_splits;
+  float* state;
+};
+
+struct FinArgs {
+  const float* state;
+  const int64_t* targets;
+  int64_t T, V, ignore_index;
+  float* loss;
+  float* lse;
+  unsigned long long* bad_counter;
+};
+
 struct GradArgs {
   const void* W;   // first row of this vocabulary chunk, [M, d]
   const void* H;   // whole H [T, d]
@@ -92,6 +112,9 @@ bool run_ws_init(unsigned long long* counter, hipStream_t s);
 bool run_fill_zero(float* p, int64_t n, hipStream_t s);
 bool run_fwd(int dtype, const FwdArgs& a, hipStream_t s);
 bool run_comb(const CombArgs& a, hipStream_t s);
+bool run_state_init(float* state, int64_t T, hipStream_t s);
+bool run_fold_merge(const FoldArgs& a, hipStream_t s);
+bool run_fold_finalize(const FinArgs& a, hipStream_t s);
 bool run_count_bad(const int64_t* targets, int64_t T, int64_t V, int64_t ignore_index,
                    unsigned long long* counter, hipStream_t s);
 // Per-XCD tile counts of one backward stage launch (dH, dW, residual tiles).

@@ -607,6 +607,50 @@ __global__ void __launch_bounds__(256) comb_kernel(CombArgs a) {
   a.loss[t] = loss;
 }
 
+// Per-shard fold (one meeting of Algorithm 2 for a state that travels with the
+// activations).  The state's m plane is kept in natural units so that it can be
+// exchanged as plain numbers; the kernels work in the base-2 domain.
+__global__ void __launch_bounds__(256) state_init_kernel(float* state, int64_t T) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= T) return;
+  state[t] = -INFINITY;
+  state[T + t] = 0.f;
+  state[2 * T + t] = 0.f;
+}
+
+// state (m, s) <- fold of state and the shard's split partials, in split order.
+__global__ void __launch_bounds__(256) fold_merge_kernel(FoldArgs a) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= a.T) return;
+  const float m_in = a.state[t];
+  float m = m_in == -INFINITY ? -INFINITY : m_in * kLog2e;
+  float s = a.state[a.T + t];
+  for (int k = 0; k < a.n_splits; ++k)
+    merge_state(m, s, a.m_part[(int64_t)k * a.T + t], a.s_part[(int64_t)k * a.T + t]);
+  a.state[t] = m == -INFINITY ? -INFINITY : m * kLn2;
+  a.state[a.T + t] = s;
+}
+
+// lse = m + log s and loss = lse - y (0 when ignored, NaN and counted when the
+// target is outside [0, V)).
+__global__ void __launch_bounds__(256) fold_finalize_kernel(FinArgs a) {
+  const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (t >= a.T) return;
+  const float lse = a.state[t] + __builtin_amdgcn_logf(a.state[a.T + t]) * kLn2;
+  const int64_t tg = a.targets[t];
+  float loss;
+  if (tg == a.ignore_index) {
+    loss = 0.f;
+  } else if (tg < 0 || tg >= a.V) {
+    loss = __builtin_nanf("");
+    atomicAdd(a.bad_counter, 1ull);
+  } else {
+    loss = lse - a.state[2 * a.T + t];
+  }
+  a.lse[t] = lse;
+  a.loss[t] = loss;
+}
+
 // Backward residual: recompute a logits tile of the (vocabulary chunk, token
 // chunk) strip and store G = g (2^(y log2e - lse log2e) - onehot) into the strip
 // in both layouts: G[v][t] (token columns contiguous, for dW) and G^T[t][v]
@@ -917,6 +961,21 @@ bool run_fwd(int dtype, const FwdArgs& a, hipStream_t s) {
 bool run_comb(const CombArgs& a, hipStream_t s) {
   const unsigned grid = (unsigned)((a.T + 255) / 256);
   hipLaunchKernelGGL(comb_kernel, dim3(grid), dim3(256), 0, s, a);
+  return launched_ok();
+}
+bool run_state_init(float* state, int64_t T, hipStream_t s) {
+  if (T <= 0) return true;
+  hipLaunchKernelGGL(state_init_kernel, dim3((unsigned)((T + 255) / 256)), dim3(256), 0, s, state, T);
+  return launched_ok();
+}
+bool run_fold_merge(const FoldArgs& a, hipStream_t s) {
+  if (a.T <= 0) return true;
+  hipLaunchKernelGGL(fold_merge_kernel, dim3((unsigned)((a.T + 255) / 256)), dim3(256), 0, s, a);
+  return launched_ok();
+}
+bool run_fold_finalize(const FinArgs& a, hipStream_t s) {
+  if (a.T <= 0) return true;
+  hipLaunchKernelGGL(fold_finalize_kernel, dim3((unsigned)((a.T + 255) / 256)), dim3(256), 0, s, a);
   return launched_ok();
 }
 bool run_count_bad(const int64_t* targets, int64_t T, int64_t V, int64_t ignore_index,

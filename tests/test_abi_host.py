@@ -171,6 +171,47 @@ def test_backward_argument_errors_before_launch():
                               1 << 30, 0) == vp.VP_ERR_ORDER
 
 
+def test_fold_argument_errors_before_launch():
+    lib = vp.load_library()
+    assert lib.vp_ce_state_init(FAKE, -1, 0) == vp.VP_ERR_SHAPE
+    assert lib.vp_ce_state_init(None, 5, 0) == vp.VP_ERR_NULL
+    assert lib.vp_ce_state_init(FAKE + 2, 5, 0) == vp.VP_ERR_ALIGN
+    assert lib.vp_ce_state_init(None, 0, 0) == vp.VP_OK
+
+    shard = _prob(shard_rows=[1000])
+    fwd_b, _ = vp.vp_ce_workspace_size(shard)
+
+    def fold(prob, off=0, H=FAKE, W=FAKE, t=FAKE, state=FAKE, ws=FAKE, ws_bytes=fwd_b):
+        return lib.vp_ce_fold_shard(ctypes.byref(prob.c), off, H, W, t, state, ws, ws_bytes, 0)
+
+    assert fold(_prob(shard_rows=[500, 500])) == vp.VP_ERR_SHAPE  # one shard per meeting
+    assert fold(shard, off=-1) == vp.VP_ERR_SHAPE
+    assert fold(shard, off=(1 << 31) - 1000) == vp.VP_ERR_SHAPE
+    assert fold(shard, ws=None) == vp.VP_ERR_WORKSPACE
+    assert fold(shard, ws_bytes=16) == vp.VP_ERR_WORKSPACE
+    assert fold(shard, ws=FAKE + 8) == vp.VP_ERR_ALIGN
+    assert fold(shard, H=None) == vp.VP_ERR_NULL
+    assert fold(shard, W=None) == vp.VP_ERR_NULL
+    assert fold(shard, t=None) == vp.VP_ERR_NULL
+    assert fold(shard, state=None) == vp.VP_ERR_NULL
+    assert fold(shard, state=FAKE + 2) == vp.VP_ERR_ALIGN
+    assert fold(shard, W=FAKE + 4) == vp.VP_ERR_ALIGN
+    # an empty shard or an empty batch is a no-op: nothing is launched
+    assert fold(_prob(shard_rows=[0]), W=None) == vp.VP_OK
+    assert fold(_prob(T=0, shard_rows=[1000]), H=None, t=None, state=None) == vp.VP_OK
+    assert fold(_prob(shard_rows=[0, 0])) == vp.VP_ERR_SHAPE
+
+    full = _prob(shard_rows=[1000, 24])
+    fin = lambda t=FAKE, state=FAKE, loss=FAKE, lse=FAKE, ws=FAKE, ws_bytes=256: \
+        lib.vp_ce_fold_finalize(ctypes.byref(full.c), t, state, loss, lse, ws, ws_bytes, 0)
+    assert fin(ws=None) == vp.VP_ERR_WORKSPACE
+    assert fin(ws_bytes=255) == vp.VP_ERR_WORKSPACE
+    assert fin(state=None) == vp.VP_ERR_NULL
+    assert fin(t=None) == vp.VP_ERR_NULL
+    assert fin(loss=None) == vp.VP_ERR_NULL
+    assert fin(state=FAKE + 1) == vp.VP_ERR_ALIGN
+
+
 def test_check_null_workspace():
     lib = vp.load_library()
     assert lib.vp_ce_check(None, None, None) == vp.VP_ERR_NULL
