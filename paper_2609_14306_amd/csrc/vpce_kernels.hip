@@ -734,37 +734,48 @@ __global__ void count_bad_kernel(const int64_t* targets, int64_t T, int64_t V, i
   }
 }
 
-// Two independent tile GEMMs with float32 outputs, C = (beta ? C : 0) + A B^T,
-// in one launch: the first tiles0 workgroups take problem 0, the rest problem
-// 1.  One launch for the dH and dW contractions of a strip halves the partly
-// filled last round of workgroups.
+// One float32 output tile of C = (beta ? C : 0) + A B^T (a dH or a dW tile; N, the
+// hidden width, is a multiple of 4).
 template <class E, class G>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int nt,
                                           typename E::storage* smem) {
   using S = typename E::storage;
-  constexpr int BM = G::BM, BN = G::BN, MB = G::MB, NB = G::NB;
+  constexpr int MB = G::MB, NB = G::NB;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = G::wave_m(wave), wn = G::wave_n(wave);
-  const int m0 = mt * BM, n0 = nt * BN;
+  // The tile is computed transposed, C^T[n][m] = sum_k B[n][k] A[m][k]: accumulator
+  // rows run along n, so each lane's group of 4 registers holds 4 consecutive
+  // columns of one row of C and the epilogue moves 16 bytes per access.
+  const int n0 = nt * G::BM, m0 = mt * G::BN;
   f32x16_t acc[MB][NB];
 #pragma unroll
   for (int i = 0; i < MB; ++i)
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
-  G::run(acc, (const S*)a.A, a.lda, m0, a.M, (const S*)a.B, a.ldb, n0, a.N, a.K, smem);
+  G::run(acc, (const S*)a.B, a.ldb, n0, a.N, (const S*)a.A, a.lda, m0, a.M, a.K, smem);
 #pragma unroll
-  for (int i = 0; i < MB; ++i)
+  for (int j = 0; j < NB; ++j) {
+    const int m = m0 + wn + 32 * j + (lane & 31);
+    if (m >= a.M) continue;
+    float* crow = a.C + (int64_t)m * a.ldc;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = m0 + wm + 32 * i + acc_row(r, lane);
-      if (m >= a.M) continue;
-      float* crow = a.C + (int64_t)m * a.ldc;
+    for (int i = 0; i < MB; ++i)
 #pragma unroll
-      for (int j = 0; j < NB; ++j) {
-        const int n = n0 + wn + 32 * j + (lane & 31);
-        if (n < a.N) crow[n] = a.beta ? crow[n] + acc[i][j][r] : acc[i][j][r];
+      for (int r4 = 0; r4 < 16; r4 += 4) {
+        const int n = n0 + wm + 32 * i + acc_row(r4, lane);  // n .. n+3; N % 4 == 0
+        if (n >= a.N) continue;
+        float4 v = make_float4(acc[i][j][r4], acc[i][j][r4 + 1], acc[i][j][r4 + 2], acc[i][j][r4 + 3]);
+        float4* p = (float4*)(crow + n);
+        if (a.beta) {
+          const float4 c = *p;
+          v.x += c.x;
+          v.y += c.y;
+          v.z += c.z;
+          v.w += c.w;
+        }
+        *p = v;
       }
-    }
+  }
 }
 
 // One launch of the backward pipeline: the dH and dW tiles of strip c and
@@ -784,14 +795,14 @@ __global__ void __launch_bounds__(GM::NT, GM::OCC)
   int local = blockIdx.x / 8;
   int mt, nt;
   if (local < sp.cnt[0][xcd]) {
-    const int n_n = (h.N + GM::BN - 1) / GM::BN, n_m = (h.M + GM::BM - 1) / GM::BM;
+    const int n_n = (h.N + GM::BM - 1) / GM::BM, n_m = (h.M + GM::BN - 1) / GM::BN;
     grouped_tile(sp.first[0][xcd] + local, n_m, n_n, 4, mt, nt);
     gemm_tile<E, GM>(h, mt, nt, smem);
     return;
   }
   local -= sp.cnt[0][xcd];
   if (local < sp.cnt[1][xcd]) {
-    const int n_n = (w.N + GM::BN - 1) / GM::BN, n_m = (w.M + GM::BM - 1) / GM::BM;
+    const int n_n = (w.N + GM::BM - 1) / GM::BM, n_m = (w.M + GM::BN - 1) / GM::BN;
     grouped_tile(sp.first[1][xcd] + local, n_m, n_n, 4, mt, nt);
     gemm_tile<E, GM>(w, mt, nt, smem);
     return;
@@ -903,8 +914,8 @@ static bool launch_stage_g(const GemmArgs& h, const GemmArgs& w, const GradArgs&
     return a.M > 0 ? ((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn) : 0;
   };
   int n_kind[3];
-  n_kind[0] = tiles(h, GM::BM, GM::BN);
-  n_kind[1] = tiles(w, GM::BM, GM::BN);
+  n_kind[0] = tiles(h, GM::BN, GM::BM);  // C^T tiles: BM along N, BN along M
+  n_kind[1] = tiles(w, GM::BN, GM::BM);
   n_kind[2] = g.M > 0 ? g.n_vt * ((g.N + GL::BN - 1) / GL::BN) : 0;
   const int n = n_kind[0] + n_kind[1] + n_kind[2];
   if (n == 0) return true;
