@@ -202,19 +202,18 @@ struct Gemm {
 //
 // Schedule of one wave (slice kt lives in ring slot kt & 1; sub-step kk covers
 // k = 16 kk .. 16 kk + 15 of the slice):
-//   sub-steps 0..2: read the fragments of sub-step kk+1 into the spare register
-//                   set, then issue the MFMAs of sub-step kk;
-//   sub-step 3:     wait for this wave's loads of slice kt+1, barrier, read the
-//                   fragments of slice kt+1 sub-step 0, issue the MFMAs of
-//                   sub-step 3, then the loads of operand A of slice kt+2 into
-//                   slot kt & 1 (every wave finished reading slice kt before the
-//                   barrier); the loads of operand B of slice kt+2 follow the
-//                   MFMAs of sub-step 0 of slice kt+1.
-// The MFMAs never wait on an LDS read issued in the same sub-step, the only
-// barrier of a slice sits where every wave still holds a sub-step of MFMAs in
-// registers, each slice's loads have three or four sub-steps of MFMAs to land,
-// and a wave stalled on issuing loads has MFMAs queued ahead of it.
-//
+//   sub-steps 0..2: issue the MFMAs of sub-step kk, each followed by one LDS read
+//                   of a fragment of sub-step kk+1 into the spare register set;
+//   sub-step 3:     wait for this wave's loads of slice kt+1, barrier, then the
+//                   MFMAs of sub-step 3 interleaved with the reads of slice kt+1
+//                   sub-step 0.
+// The loads of slice kt+2 go out one per two MFMAs, half during sub-step 3 of
+// slice kt (into slot kt & 1: every wave finished reading slice kt before the
+// barrier) and half during sub-step 0 of slice kt+1.  The MFMAs never wait on an
+// LDS read issued in the same sub-step, the only barrier of a slice sits where
+// every wave holds a sub-step of fragments in registers, each slice's loads have
+// three or four sub-steps of MFMAs to land, and no burst of memory instructions
+// ever stands in front of a wave's next MFMA.
 // The loads are issued from inline assembly with a scalar base (the tile's
 // first row at the slice's k offset) and a 32-bit per-lane byte offset, so that
 // the compiler neither drains the loads before each LDS read (it cannot tell
@@ -251,6 +250,15 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 __device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
+// One load on its own, with the same wait states.
+__device__ __forceinline__ void lds_dma16x1(const void* sbase, uint32_t o0, uint32_t l0) {
+  uint32_t m0v = l0;
+  asm volatile("s_nop 4\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
+               : "+{m0}"(m0v)
+               : "v"(o0), "s"(sbase)
+               : "memory");
+}
+
 template <int BM_, int BN_, int WGM_, int WGN_>
 struct GemmDma {
   using S = uint16_t;
@@ -274,6 +282,9 @@ struct GemmDma {
   static constexpr int A_LOADS = BM / RPI / NWAVES;  // load instructions per wave and slice
   static constexpr int B_LOADS = BN / RPI / NWAVES;
   static_assert(A_LOADS % 4 == 0 && B_LOADS % 4 == 0, "loads are issued in blocks of four");
+  static constexpr int NLOADS = A_LOADS + B_LOADS;  // per wave and slice
+  static constexpr int NM = MB * NB, NR = MB + NB;   // MFMAs and fragment reads per sub-step
+  static_assert(NR <= NM && NLOADS / 2 <= (NM + 1) / 2, "interleave slots");
   static constexpr int LDS_ELEMS = 2 * SLICE_BYTES / 2;
 
   // Chunk c of slice row r lives in slot c ^ key(r): within one 256-byte window
@@ -334,6 +345,25 @@ struct GemmDma {
                   l + (q + 1) * STEP, l + (q + 2) * STEP, l + (q + 3) * STEP);
   }
 
+  // Load q (operand A's loads, then B's) of slice kt on its own.
+  __device__ __forceinline__ static void issue_one(const Loads& L, int kt, int q, uint32_t lds0,
+                                                   int wave) {
+    const int64_t kb = (int64_t)kt * ROW_BYTES;
+    const uint32_t l = lds0 + (uint32_t)((kt & 1) * SLICE_BYTES + wave * 1024) + q * NWAVES * 1024;
+    if (q < A_LOADS)
+      lds_dma16x1(L.baseA + kb, L.offA[q], l);
+    else
+      lds_dma16x1(L.baseB + kb, L.offB[q - A_LOADS], l);
+  }
+
+  // Fragment idx (the MB A blocks, then the NB B blocks) of sub-step kk at `slot`.
+  __device__ __forceinline__ static bf16x8_t read_one(const S* slot, int wm, int wn, int kk,
+                                                      int lane, int idx) {
+    const int chunk = 2 * kk + (lane >> 5);
+    const int row = idx < MB ? wm + 32 * idx + (lane & 31) : BM + wn + 32 * (idx - MB) + (lane & 31);
+    return *(const bf16x8_t*)(slot + row * BK + ((chunk ^ key(row)) << 3));
+  }
+
   // Fragments of sub-step kk of the slice at `slot`: lane l takes row l % 32 of
   // each 32-row block and k = 16 kk + 8 (l / 32) + 0..7, i.e. chunk 2 kk + l / 32.
   __device__ __forceinline__ static void read(bf16x8_t (&a)[MB], bf16x8_t (&b)[NB], const S* slot,
@@ -349,15 +379,6 @@ struct GemmDma {
       const int row = BM + wn + 32 * j + (lane & 31);
       b[j] = *(const bf16x8_t*)(slot + row * BK + ((chunk ^ key(row)) << 3));
     }
-  }
-
-  __device__ __forceinline__ static void mma(f32x16_t (&acc)[MB][NB], const bf16x8_t (&a)[MB],
-                                             const bf16x8_t (&b)[NB]) {
-#pragma unroll
-    for (int i = 0; i < MB; ++i)
-#pragma unroll
-      for (int j = 0; j < NB; ++j)
-        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
   }
 
   // acc += A[m0 : m0+BM, 0:K] B[n0 : n0+BN, 0:K]^T; requires m0 < M and n0 < N.
@@ -384,34 +405,58 @@ struct GemmDma {
     bf16x8_t a[2][MB], b[2][NB];
     read(a[0], b[0], smem, wm, wn, 0, lane);
     for (int kt = 0; kt < nk; ++kt) {
-      const S* slot = smem + (kt & 1) * (SLICE_BYTES / 2);
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
         const int cur = kk & 1;
+        // where the fragments of the next sub-step come from
+        const S* src;
+        int skk;
         if (kk + 1 < NKK) {
-          read(a[cur ^ 1], b[cur ^ 1], slot, wm, wn, kk + 1, lane);
+          src = smem + (kt & 1) * (SLICE_BYTES / 2);
+          skk = kk + 1;
         } else {
           // Taken on the last slice too (one spare barrier, fragments read from
           // the idle slot and never used): no branch around the LDS reads, so
-          // the compiler's count of reads in flight stays exact and the MFMAs
-          // below wait only for the reads of this slice.
+          // the compiler's count of reads in flight stays exact.
           wait_vmcnt<0>();  // this wave's loads of slice kt+1
           wait_lgkmcnt0();  // this wave's reads of slice kt
           __builtin_amdgcn_s_barrier();
-          read(a[cur ^ 1], b[cur ^ 1], smem + ((kt + 1) & 1) * (SLICE_BYTES / 2), wm, wn, 0, lane);
+          src = smem + ((kt + 1) & 1) * (SLICE_BYTES / 2);
+          skk = 0;
         }
-        __builtin_amdgcn_sched_barrier(0);
-        mma(acc, a[cur], b[cur]);
-        __builtin_amdgcn_sched_barrier(0);
-        // The loads of slice kt+2 go out in two halves behind MFMAs already issued:
-        // operand A after the last sub-step of slice kt, operand B after the first
+        // The loads of slice kt+2 go out in two halves: the first half during the
+        // last sub-step of slice kt (after the barrier: every wave has finished
+        // reading slice kt, whose slot they refill), the second during the first
         // sub-step of slice kt+1 (slice 1 came whole from the prologue).
-        if (kk == NKK - 1 && kt + 2 < nk) issue<0>(L, kt + 2, lds0, wave);
-        if (kk == 0 && kt >= 1 && kt + 1 < nk) issue<1>(L, kt + 1, lds0, wave);
+        constexpr int HALF = NLOADS / 2;
+        const int dq0 = kk == NKK - 1 ? 0 : HALF;
+        const int dslice = kk == NKK - 1 ? kt + 2 : kt + 1;
+        const bool dvalid = (kk == NKK - 1 && kt + 2 < nk) || (kk == 0 && kt >= 1 && kt + 1 < nk);
         __builtin_amdgcn_sched_barrier(0);
+        // One MFMA, then one fragment read for the next sub-step, then (every other
+        // MFMA) one load: the wave never holds a burst of memory instructions in
+        // front of its next MFMA.
+#pragma unroll
+        for (int idx = 0; idx < NM; ++idx) {
+          const int i = idx / NB, j = idx % NB;
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cur][i], b[cur][j], acc[i][j], 0, 0, 0);
+          __builtin_amdgcn_sched_barrier(0);
+          if (idx < NR) {
+            const bf16x8_t f = read_one(src, wm, wn, skk, lane, idx);
+            if (idx < MB)
+              a[cur ^ 1][idx] = f;
+            else
+              b[cur ^ 1][idx - MB] = f;
+          }
+          if ((idx & 1) == 0 && idx / 2 < HALF && (kk == NKK - 1 || kk == 0) && dvalid)
+            issue_one(L, dslice, dq0 + idx / 2, lds0, wave);
+          __builtin_amdgcn_sched_barrier(0);
+        }
       }
     }
-    // no wave may still be reading the ring when the caller reuses LDS
+    // no wave may still be reading the ring, nor a load writing it, when the caller
+    // reuses LDS
+    wait_vmcnt<0>();
     wait_lgkmcnt0();
     __builtin_amdgcn_s_barrier();
   }
