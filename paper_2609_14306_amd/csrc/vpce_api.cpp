@@ -402,8 +402,12 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
   void* Ht = wsb + plan.off_ht;
   void* Wt = wsb + plan.off_wt;
   const size_t eb = elem_bytes(prob->dtype);
+  // bfloat16 workspaces (the residual strips, H^T and W^T) are k-blocked: every
+  // 64-deep slice of a 256-row tile the dH / dW contractions stream is one
+  // contiguous 32 KiB block; float32 ones are row-major.
+  const int32_t blocked = prob->dtype == VP_BF16 ? 1 : 0;
 
-  {  // H^T [d][T_pad], zero beyond T
+  {  // H^T [d][T_pad] (k-blocked: [T_pad/64][d][64]), zero beyond T
     vpce::TransposeArgs tr;
     tr.in = H;
     tr.ld_in = d;
@@ -412,6 +416,7 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
     tr.R = (int32_t)T;
     tr.C = (int32_t)d;
     tr.R_pad = (int32_t)plan.T_pad;
+    tr.blocked = blocked;
     if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
   }
 
@@ -442,8 +447,8 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
       g.grad = grad_loss;
       g.strip = wsb + plan.off_g[k % 2];
       g.strip_t = wsb + plan.off_gt[k % 2];
-      g.ldg = plan.Tc;
-      g.ldgt = plan.Vc;
+      g.Tc = plan.Tc;
+      g.Vc = plan.Vc;
       g.t0 = c.t0;
       g.gid0 = off[c.q] + c.v0;
       g.V = V;
@@ -467,13 +472,16 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
         tr.R = (int32_t)c.M;
         tr.C = (int32_t)d;
         tr.R_pad = (int32_t)round_up(c.M, 64);  // >= the K the dH launch reads
+        tr.blocked = blocked;
         if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
       }
       // dH[t0 : t0+N] (+)= G^T W_chunk = G^T . (W^T)^T
       h.A = wsb + plan.off_gt[(k - 1) % 2];
-      h.lda = plan.Vc;
+      h.lda = blocked ? 64 : plan.Vc;
+      h.kblka = blocked ? plan.Tc * 64 : 64;
       h.B = Wt;
-      h.ldb = plan.Vc;
+      h.ldb = blocked ? 64 : plan.Vc;
+      h.kblkb = blocked ? d * 64 : 64;
       h.C = dH + c.t0 * d;
       h.ldc = d;
       h.M = (int32_t)c.N;
@@ -482,9 +490,11 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
       h.beta = c.first_vchunk ? 0 : 1;
       // dW_chunk (+)= G H[t0 : t0+N] = G . (H^T)^T
       w.A = wsb + plan.off_g[(k - 1) % 2];
-      w.lda = plan.Tc;
-      w.B = (const char*)Ht + (size_t)c.t0 * eb;
-      w.ldb = plan.T_pad;
+      w.lda = blocked ? 64 : plan.Tc;
+      w.kblka = blocked ? plan.Vc * 64 : 64;
+      w.B = (const char*)Ht + (size_t)(blocked ? (c.t0 / 64) * d * 64 : c.t0) * eb;
+      w.ldb = blocked ? 64 : plan.T_pad;
+      w.kblkb = blocked ? d * 64 : 64;
       w.C = dW_shards[c.q] + c.v0 * d;
       w.ldc = d;
       w.M = (int32_t)c.M;

@@ -68,9 +68,15 @@ struct GradArgs {
   const int64_t* targets;
   const float* lse;
   const float* grad;
-  void* strip;     // G   [Vc][ldg]  (token columns contiguous)
-  void* strip_t;   // G^T [Tc][ldgt] (vocabulary columns contiguous)
-  int64_t ldg, ldgt;
+  // The residual strip in two layouts, Tc tokens by Vc vocabulary rows each:
+  //   float32: G [Vc][Tc] and G^T [Tc][Vc], row-major;
+  //   bfloat16: k-blocked, G [Tc/64][Vc][64] (element (v, t) at
+  //   ((t / 64) Vc + v) 64 + t % 64) and G^T [Vc/64][Tc][64] (element (t, v) at
+  //   ((v / 64) Tc + t) 64 + v % 64), so that a 64-deep slice of a 256-row tile
+  //   of either operand is one contiguous 32 KiB block.
+  void* strip;
+  void* strip_t;
+  int64_t Tc, Vc;
   int64_t t0;      // first token of this chunk
   int64_t gid0;    // global id of the chunk's first row
   int64_t V, ignore_index;
@@ -91,15 +97,22 @@ struct GemmArgs {
   int64_t ldc;
   int32_t M, N, K;
   int32_t beta;
+  // elements between consecutive 64-wide k blocks of A and of B: 64 for a
+  // row-major operand, rows * 64 for a k-blocked one (whose row pitch is 64)
+  int64_t kblka, kblkb;
 };
 
 // out[c][r] = in[r][c] for r < R, c < C; out[c][r] = 0 for R <= r < R_pad.
+// out[c][r] = in[r][c] for r < R (zero for R <= r < R_pad), c < C.  blocked == 0:
+// out is row-major with pitch ld_out; blocked != 0: out is k-blocked,
+// [R_pad/64][C][64] (element (c, r) at ((r / 64) C + c) 64 + r % 64).
 struct TransposeArgs {
   const void* in;
   int64_t ld_in;
   void* out;
   int64_t ld_out;
   int32_t R, C, R_pad;
+  int32_t blocked;
 };
 
 struct TileShape {

@@ -135,9 +135,11 @@ struct Gemm {
   __device__ __forceinline__ static int wave_m(int wave) { return (wave / WGN) * WM; }
   __device__ __forceinline__ static int wave_n(int wave) { return (wave % WGN) * WN; }
 
+  // Row-major operands only (the k-block strides are for the direct-load tile).
   __device__ __forceinline__ static void run(f32x16_t (&acc)[MB][NB], const S* __restrict__ A,
                                              int64_t lda, int m0, int M, const S* __restrict__ B,
-                                             int64_t ldb, int n0, int N, int K, S* smem) {
+                                             int64_t ldb, int n0, int N, int K, S* smem,
+                                             int64_t = 64, int64_t = 64) {
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     const int wm = wave_m(wave), wn = wave_n(wave);
     SA la;
@@ -259,18 +261,18 @@ __device__ __forceinline__ void lds_dma16x1(const void* sbase, uint32_t o0, uint
                : "memory");
 }
 
-template <int BM_, int BN_, int WGM_, int WGN_>
+template <int BM_, int BN_, int WGM_, int WGN_, int BK_ = 64, int STAGES_ = 2>
 struct GemmDma {
   using S = uint16_t;
   static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
   static constexpr int NT = 64 * WGM * WGN, NWAVES = WGM * WGN;
-  // One workgroup per CU (the ring takes 128 KiB of LDS): 512 threads run two
-  // wavefronts per SIMD with 256 registers each, 256 threads one wavefront per
-  // SIMD with 512 (256 of them accumulation registers).
+  // One workgroup per CU (the ring takes 128 to 160 KiB of LDS): 512 threads run
+  // two wavefronts per SIMD with 256 registers each.
   static constexpr int OCC = 1;
   static constexpr int WM = BM / WGM, WN = BN / WGN, MB = WM / 32, NB = WN / 32;
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be whole 32x32 blocks");
-  static constexpr int BK = 64;
+  static constexpr int BK = BK_, STAGES = STAGES_;
+  static_assert((BK == 32 || BK == 64) && STAGES >= 2, "slice depth and ring slots");
   static constexpr int KDIV = BK;                 // K must be a multiple of the slice depth
   static constexpr int NKK = BK / 16;             // MFMA sub-steps per slice
   static_assert(NKK % 2 == 0, "register sets alternate per sub-step across slices");
@@ -281,11 +283,13 @@ struct GemmDma {
   static constexpr int SLICE_BYTES = (BM + BN) * ROW_BYTES;
   static constexpr int A_LOADS = BM / RPI / NWAVES;  // load instructions per wave and slice
   static constexpr int B_LOADS = BN / RPI / NWAVES;
-  static_assert(A_LOADS % 4 == 0 && B_LOADS % 4 == 0, "loads are issued in blocks of four");
+  static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "whole load groups per wave");
   static constexpr int NLOADS = A_LOADS + B_LOADS;  // per wave and slice
+  static_assert(NLOADS % 2 == 0, "loads go out in two halves");
   static constexpr int NM = MB * NB, NR = MB + NB;   // MFMAs and fragment reads per sub-step
   static_assert(NR <= NM && NLOADS / 2 <= (NM + 1) / 2, "interleave slots");
-  static constexpr int LDS_ELEMS = 2 * SLICE_BYTES / 2;
+  static constexpr int LDS_ELEMS = STAGES * SLICE_BYTES / 2;
+  static_assert(LDS_ELEMS * 2 <= 160 * 1024, "LDS");
 
   // Chunk c of slice row r lives in slot c ^ key(r): within one 256-byte window
   // the rows sit at distinct offsets, and key(r) differs for the CPR rows that
@@ -296,6 +300,10 @@ struct GemmDma {
   __device__ __forceinline__ static int wave_m(int wave) { return (wave / WGN) * WM; }
   __device__ __forceinline__ static int wave_n(int wave) { return (wave % WGN) * WN; }
 
+  __device__ __forceinline__ static uint32_t slot_bytes(int kt) {
+    return (uint32_t)((kt % STAGES) * SLICE_BYTES);
+  }
+
   // Load instruction q of a wave covers the RPI slice rows starting at
   // (wave + q * NWAVES) * RPI; A rows come first.  Rows at or beyond M (N) are
   // clamped to the last row: they only feed accumulator rows (columns) that are
@@ -303,6 +311,7 @@ struct GemmDma {
   struct Loads {
     const char* baseA;  // byte address of the tile's first A row (k = 0)
     const char* baseB;
+    int64_t kblkA, kblkB;  // elements between consecutive 64-wide k blocks
     uint32_t offA[A_LOADS], offB[B_LOADS];  // per-lane byte offsets from the bases
   };
 
@@ -327,36 +336,21 @@ struct GemmDma {
     }
   }
 
-  // Issue this wave's loads of one operand of slice kt into ring slot kt & 1: load
-  // q of operand A fills the 1 KiB at (wave + q * NWAVES) KiB of the slot, load q
-  // of operand B the 1 KiB at (wave + (A_LOADS + q) * NWAVES) KiB.
-  template <int OP>
-  __device__ __forceinline__ static void issue(const Loads& L, int kt, uint32_t lds0, int wave) {
-    const int64_t kb = (int64_t)kt * ROW_BYTES;
-    constexpr uint32_t STEP = NWAVES * 1024;
-    constexpr int NL = OP == 0 ? A_LOADS : B_LOADS;
-    const char* base = (OP == 0 ? L.baseA : L.baseB) + kb;
-    const uint32_t* off = OP == 0 ? L.offA : L.offB;
-    const uint32_t l = lds0 + (uint32_t)((kt & 1) * SLICE_BYTES + wave * 1024) +
-                       (OP == 0 ? 0u : A_LOADS * STEP);
-#pragma unroll
-    for (int q = 0; q < NL; q += 4)
-      lds_dma16x4(base, off[q], off[q + 1], off[q + 2], off[q + 3], l + q * STEP,
-                  l + (q + 1) * STEP, l + (q + 2) * STEP, l + (q + 3) * STEP);
-  }
-
-  // Load q (operand A's loads, then B's) of slice kt on its own.
+  // Load q (operand A's loads, then B's) of slice kt, into ring slot kt % STAGES:
+  // it fills the 1 KiB at (wave + q * NWAVES) KiB of the slot.
   __device__ __forceinline__ static void issue_one(const Loads& L, int kt, int q, uint32_t lds0,
                                                    int wave) {
-    const int64_t kb = (int64_t)kt * ROW_BYTES;
-    const uint32_t l = lds0 + (uint32_t)((kt & 1) * SLICE_BYTES + wave * 1024) + q * NWAVES * 1024;
+    const int64_t k0 = (int64_t)kt * BK;
+    const uint32_t l = lds0 + slot_bytes(kt) + (uint32_t)(wave * 1024) + q * NWAVES * 1024;
     if (q < A_LOADS)
-      lds_dma16x1(L.baseA + kb, L.offA[q], l);
+      lds_dma16x1(L.baseA + ((k0 >> 6) * L.kblkA + (k0 & 63)) * 2, L.offA[q], l);
     else
-      lds_dma16x1(L.baseB + kb, L.offB[q - A_LOADS], l);
+      lds_dma16x1(L.baseB + ((k0 >> 6) * L.kblkB + (k0 & 63)) * 2, L.offB[q - A_LOADS], l);
   }
 
-  // Fragment idx (the MB A blocks, then the NB B blocks) of sub-step kk at `slot`.
+  // Fragment idx (the MB A blocks, then the NB B blocks) of sub-step kk at `slot`:
+  // lane l takes row l % 32 of the block and k = 16 kk + 8 (l / 32) + 0..7, i.e.
+  // chunk 2 kk + l / 32.
   __device__ __forceinline__ static bf16x8_t read_one(const S* slot, int wm, int wn, int kk,
                                                       int lane, int idx) {
     const int chunk = 2 * kk + (lane >> 5);
@@ -364,28 +358,32 @@ struct GemmDma {
     return *(const bf16x8_t*)(slot + row * BK + ((chunk ^ key(row)) << 3));
   }
 
-  // Fragments of sub-step kk of the slice at `slot`: lane l takes row l % 32 of
-  // each 32-row block and k = 16 kk + 8 (l / 32) + 0..7, i.e. chunk 2 kk + l / 32.
-  __device__ __forceinline__ static void read(bf16x8_t (&a)[MB], bf16x8_t (&b)[NB], const S* slot,
-                                              int wm, int wn, int kk, int lane) {
-    const int chunk = 2 * kk + (lane >> 5);
-#pragma unroll
-    for (int i = 0; i < MB; ++i) {
-      const int row = wm + 32 * i + (lane & 31);
-      a[i] = *(const bf16x8_t*)(slot + row * BK + ((chunk ^ key(row)) << 3));
-    }
-#pragma unroll
-    for (int j = 0; j < NB; ++j) {
-      const int row = BM + wn + 32 * j + (lane & 31);
-      b[j] = *(const bf16x8_t*)(slot + row * BK + ((chunk ^ key(row)) << 3));
+  // Wait until at most n slices' loads (n in [0, STAGES - 1]) of this wave are in
+  // flight; loads return in issue order.
+  __device__ __forceinline__ static void wait_slices(int n) {
+    if constexpr (STAGES == 2) {
+      if (n <= 0) wait_vmcnt<0>(); else wait_vmcnt<NLOADS>();
+    } else {
+      static_assert(STAGES <= 5, "wait_slices covers up to five slots");
+      switch (n) {
+        case 0: wait_vmcnt<0>(); break;
+        case 1: wait_vmcnt<NLOADS>(); break;
+        case 2: wait_vmcnt<2 * NLOADS>(); break;
+        case 3: wait_vmcnt<3 * NLOADS>(); break;
+        default: wait_vmcnt<4 * NLOADS>(); break;
+      }
     }
   }
 
   // acc += A[m0 : m0+BM, 0:K] B[n0 : n0+BN, 0:K]^T; requires m0 < M and n0 < N.
+  // Element (r, k) of A is at A[(k / 64) kblka + r lda + k % 64] (row-major:
+  // kblka = 64; k-blocked: lda = 64, kblka = rows * 64), likewise for B.
   // LDS is free again for the caller when run() returns.
   __device__ __forceinline__ static void run(f32x16_t (&acc)[MB][NB], const S* __restrict__ A,
                                              int64_t lda, int m0, int M, const S* __restrict__ B,
-                                             int64_t ldb, int n0, int N, int K, S* smem) {
+                                             int64_t ldb, int n0, int N, int K, S* smem,
+                                             int64_t kblka = 64, int64_t kblkb = 64) {
+    // The wave index is made scalar so that every branch on it is a scalar branch.
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int wm = wave_m(wave), wn = wave_n(wave);
@@ -394,16 +392,24 @@ struct GemmDma {
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) S*)smem;
     Loads L;
     plan(L, A, lda, m0, M, B, ldb, n0, N, wave, lane);
-    issue<0>(L, 0, lds0, wave);
-    issue<1>(L, 0, lds0, wave);
-    wait_vmcnt<0>();
+    L.kblkA = kblka;
+    L.kblkB = kblkb;
+    // prologue: the first min(STAGES, nk) slices, whole; wait for slice 0
+    const int pro = min(STAGES, nk);
+    for (int kt = 0; kt < pro; ++kt)
+#pragma unroll
+      for (int q = 0; q < NLOADS; ++q) issue_one(L, kt, q, lds0, wave);
+    wait_slices(pro - 1);
     __builtin_amdgcn_s_barrier();
-    if (nk > 1) {
-      issue<0>(L, 1, lds0, wave);
-      issue<1>(L, 1, lds0, wave);
-    }
     bf16x8_t a[2][MB], b[2][NB];
-    read(a[0], b[0], smem, wm, wn, 0, lane);
+#pragma unroll
+    for (int idx = 0; idx < NR; ++idx) {
+      const bf16x8_t f = read_one(smem, wm, wn, 0, lane, idx);
+      if (idx < MB)
+        a[0][idx] = f;
+      else
+        b[0][idx - MB] = f;
+    }
     for (int kt = 0; kt < nk; ++kt) {
 #pragma unroll
       for (int kk = 0; kk < NKK; ++kk) {
@@ -412,26 +418,27 @@ struct GemmDma {
         const S* src;
         int skk;
         if (kk + 1 < NKK) {
-          src = smem + (kt & 1) * (SLICE_BYTES / 2);
+          src = smem + slot_bytes(kt) / 2;
           skk = kk + 1;
         } else {
-          // Taken on the last slice too (one spare barrier, fragments read from
-          // the idle slot and never used): no branch around the LDS reads, so
-          // the compiler's count of reads in flight stays exact.
-          wait_vmcnt<0>();  // this wave's loads of slice kt+1
+          // Slice kt+1 must have landed; slices kt+2 .. kt+STAGES-1 may still be
+          // in flight.  Taken on the last slice too (one spare barrier, fragments
+          // read from an idle slot and never used): no branch around the LDS
+          // reads, so the compiler's count of reads in flight stays exact.
+          wait_slices(min(STAGES - 2, nk - 2 - kt));
           wait_lgkmcnt0();  // this wave's reads of slice kt
           __builtin_amdgcn_s_barrier();
-          src = smem + ((kt + 1) & 1) * (SLICE_BYTES / 2);
+          src = smem + slot_bytes(kt + 1) / 2;
           skk = 0;
         }
-        // The loads of slice kt+2 go out in two halves: the first half during the
+        // The loads of slice kt+STAGES go out in two halves: the first during the
         // last sub-step of slice kt (after the barrier: every wave has finished
         // reading slice kt, whose slot they refill), the second during the first
-        // sub-step of slice kt+1 (slice 1 came whole from the prologue).
+        // sub-step of slice kt+1 (the prologue issued the first STAGES slices).
         constexpr int HALF = NLOADS / 2;
         const int dq0 = kk == NKK - 1 ? 0 : HALF;
-        const int dslice = kk == NKK - 1 ? kt + 2 : kt + 1;
-        const bool dvalid = (kk == NKK - 1 && kt + 2 < nk) || (kk == 0 && kt >= 1 && kt + 1 < nk);
+        const int dslice = kk == NKK - 1 ? kt + STAGES : kt + STAGES - 1;
+        const bool dvalid = (kk == NKK - 1 || (kk == 0 && kt >= 1)) && dslice < nk;
         __builtin_amdgcn_sched_barrier(0);
         // One MFMA, then one fragment read for the next sub-step, then (every other
         // MFMA) one load: the wave never holds a burst of memory instructions in
@@ -719,9 +726,11 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
   G::run(acc, (const S*)a.W, a.d, m0, a.M, (const S*)a.H + a.t0 * a.d, a.d, n0, a.N, a.d, smem);
 
   // Strip offsets fit in 32 bits (the strip budget is capped below 2^31 elements).
+  // bfloat16 strips are k-blocked, float32 strips row-major (see GradArgs).
+  constexpr bool kBlocked = sizeof(S) == 2;
   S* __restrict__ Gs = (S*)a.strip;
   S* __restrict__ Gt = (S*)a.strip_t;
-  const uint32_t ldg = (uint32_t)a.ldg, ldgt = (uint32_t)a.ldgt;
+  const uint32_t Tc = (uint32_t)a.Tc, Vc = (uint32_t)a.Vc;
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int nl = n0 + wn + 32 * j + (lane & 31);  // token column within the chunk
@@ -754,9 +763,13 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r4 + q], kLog2e, -lse2));
           const float v = (live && ml < a.M) ? g * (p - (rel == ml ? 1.f : 0.f)) : 0.f;
           v4[q] = E::from_f32(v);
-          Gs[(uint32_t)ml * ldg + (uint32_t)nl] = v4[q];
+          Gs[kBlocked ? (((uint32_t)nl >> 6) * Vc + (uint32_t)ml) * 64u + ((uint32_t)nl & 63u)
+                      : (uint32_t)ml * Tc + (uint32_t)nl] = v4[q];
         }
-        const uint32_t ot = (uint32_t)nl * ldgt + (uint32_t)ml0;
+        // 4 consecutive vocabulary rows (ml0 % 4 == 0: one 64-wide block)
+        const uint32_t ot = kBlocked ? (((uint32_t)ml0 >> 6) * Tc + (uint32_t)nl) * 64u +
+                                           ((uint32_t)ml0 & 63u)
+                                     : (uint32_t)nl * Vc + (uint32_t)ml0;
         if constexpr (sizeof(S) == 2) {
           uint2 packed;
           packed.x = (uint32_t)v4[0] | ((uint32_t)v4[1] << 16);
@@ -797,7 +810,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int nt,
   for (int i = 0; i < MB; ++i)
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
-  G::run(acc, (const S*)a.B, a.ldb, n0, a.N, (const S*)a.A, a.lda, m0, a.M, a.K, smem);
+  G::run(acc, (const S*)a.B, a.ldb, n0, a.N, (const S*)a.A, a.lda, m0, a.M, a.K, smem, a.kblkb,
+         a.kblka);
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int m = m0 + wn + 32 * j + (lane & 31);
@@ -874,7 +888,11 @@ __global__ void __launch_bounds__(256) transpose_kernel(TransposeArgs a) {
   __syncthreads();
   for (int i = ty; i < 64; i += 4) {
     const int c = c0 + i, r = r0 + tx;
-    if (c < a.C && r < a.R_pad) out[(int64_t)c * a.ld_out + r] = tile[tx][i];
+    if (c < a.C && r < a.R_pad) {
+      const int64_t o = a.blocked ? ((int64_t)(r >> 6) * a.C + c) * 64 + (r & 63)
+                                  : (int64_t)c * a.ld_out + r;
+      out[o] = tile[tx][i];
+    }
   }
 }
 
