@@ -703,12 +703,41 @@ __global__ void __launch_bounds__(256) fold_finalize_kernel(FinArgs a) {
   a.loss[t] = loss;
 }
 
+// Byte offset of element (row, col) of a 256 x 256 bfloat16 tile staged in LDS as
+// four 64-column blocks of 256 rows x 128 bytes, the 16-byte chunks of each row
+// XOR-swizzled by (row / 2) % 8 so that the rows a write or read phase touches
+// spread over the banks.  Each block is laid out exactly like the matching
+// 32 KiB block of a k-blocked strip.
+__device__ __forceinline__ uint32_t tile_lds_byte(int row, int col) {
+  return (uint32_t)((col >> 6) * 32768 + row * 128 + ((((col & 63) >> 3) ^ ((row >> 1) & 7)) << 4) +
+                    (col & 7) * 2);
+}
+
+// Copies the 256 x 256 bfloat16 tile staged in LDS (see tile_lds_byte) to a
+// k-blocked strip: block b (columns 64 b .. 64 b + 63) goes to the 32 KiB at
+// element ((kb0 + b) * rows_pitch + r0) * 64, one 16-byte chunk per thread and
+// step, 1 KiB contiguous per wavefront store.
+template <int NT>
+__device__ __forceinline__ void store_tile_blocked(const uint16_t* lds, uint16_t* __restrict__ dst,
+                                                   uint32_t kb0, uint32_t rows_pitch, uint32_t r0) {
+  const int tid = threadIdx.x;
+#pragma unroll
+  for (int q = 0; q < 8192 / NT; ++q) {
+    const int c = q * NT + tid;  // 16-byte chunk of the tile
+    const int b = c >> 11, row = (c >> 3) & 255, ch = c & 7;
+    const uint4 v = *(const uint4*)((const char*)lds + b * 32768 + row * 128 + ((ch ^ ((row >> 1) & 7)) << 4));
+    *(uint4*)(dst + (((kb0 + (uint32_t)b) * rows_pitch + r0 + (uint32_t)row) * 64u + (uint32_t)ch * 8u)) = v;
+  }
+}
+
 // Backward residual: recompute a logits tile of the (vocabulary chunk, token
 // chunk) strip and store G = g (2^(y log2e - lse log2e) - onehot) into the strip
 // in both layouts: G[v][t] (token columns contiguous, for dW) and G^T[t][v]
 // (vocabulary columns contiguous, for dH).  Rows and columns of the tile that
 // fall outside the chunk are written as zeros so that both contractions can
-// read whole 16-byte chunks past a ragged edge.
+// read whole 16-byte chunks past a ragged edge.  bfloat16 tiles go through LDS
+// (free once the mainloop returns) once per layout, so that both layouts leave
+// as whole 16-byte chunks, 1 KiB per wavefront store.
 template <class E, class G>
 __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
                                           typename E::storage* smem) {
@@ -731,6 +760,13 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
   S* __restrict__ Gs = (S*)a.strip;
   S* __restrict__ Gt = (S*)a.strip_t;
   const uint32_t Tc = (uint32_t)a.Tc, Vc = (uint32_t)a.Vc;
+  if constexpr (kBlocked) {
+    static_assert(BM == 256 && BN == 256, "the LDS staging holds one 256 x 256 tile");
+    static_assert(G::LDS_ELEMS >= BM * BN, "the ring must hold one bfloat16 tile");
+  }
+  // G values of this lane, bfloat16 bits packed two per word: packed[j][i][r4/4]
+  // holds vocabulary rows ml0 .. ml0 + 3 of token column nl.
+  uint2 packed[NB][MB][4];
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int nl = n0 + wn + 32 * j + (lane & 31);  // token column within the chunk
@@ -763,22 +799,49 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r4 + q], kLog2e, -lse2));
           const float v = (live && ml < a.M) ? g * (p - (rel == ml ? 1.f : 0.f)) : 0.f;
           v4[q] = E::from_f32(v);
-          Gs[kBlocked ? (((uint32_t)nl >> 6) * Vc + (uint32_t)ml) * 64u + ((uint32_t)nl & 63u)
-                      : (uint32_t)ml * Tc + (uint32_t)nl] = v4[q];
+          if constexpr (!kBlocked) Gs[(uint32_t)ml * Tc + (uint32_t)nl] = v4[q];
         }
-        // 4 consecutive vocabulary rows (ml0 % 4 == 0: one 64-wide block)
-        const uint32_t ot = kBlocked ? (((uint32_t)ml0 >> 6) * Tc + (uint32_t)nl) * 64u +
-                                           ((uint32_t)ml0 & 63u)
-                                     : (uint32_t)nl * Vc + (uint32_t)ml0;
-        if constexpr (sizeof(S) == 2) {
-          uint2 packed;
-          packed.x = (uint32_t)v4[0] | ((uint32_t)v4[1] << 16);
-          packed.y = (uint32_t)v4[2] | ((uint32_t)v4[3] << 16);
-          *(uint2*)(Gt + ot) = packed;
+        if constexpr (kBlocked) {
+          packed[j][i][r4 >> 2].x = (uint32_t)v4[0] | ((uint32_t)v4[1] << 16);
+          packed[j][i][r4 >> 2].y = (uint32_t)v4[2] | ((uint32_t)v4[3] << 16);
         } else {
-          *(float4*)(Gt + ot) = make_float4(v4[0], v4[1], v4[2], v4[3]);
+          *(float4*)(Gt + (uint32_t)nl * Vc + (uint32_t)ml0) = make_float4(v4[0], v4[1], v4[2], v4[3]);
         }
       }
+  }
+  if constexpr (kBlocked) {
+    uint16_t* lds = (uint16_t*)smem;
+    // G^T: the tile as rows of tokens, columns of vocabulary ids; a lane's 4
+    // consecutive ids are one 8-byte write.
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int r4 = 0; r4 < 16; r4 += 4) {
+          const int tl = wn + 32 * j + (lane & 31), vl = wm + 32 * i + acc_row(r4, lane);
+          *(uint2*)((char*)lds + tile_lds_byte(tl, vl)) = packed[j][i][r4 >> 2];
+        }
+    __syncthreads();
+    store_tile_blocked<G::NT>(lds, Gt, (uint32_t)m0 >> 6, Tc, (uint32_t)n0);
+    __syncthreads();
+    // G: the tile as rows of vocabulary ids, columns of tokens.
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+#pragma unroll
+      for (int i = 0; i < MB; ++i)
+#pragma unroll
+        for (int r4 = 0; r4 < 16; r4 += 4) {
+          const int tl = wn + 32 * j + (lane & 31), vl = wm + 32 * i + acc_row(r4, lane);
+          const uint2 p = packed[j][i][r4 >> 2];
+          char* base = (char*)lds;
+          *(uint16_t*)(base + tile_lds_byte(vl, tl)) = (uint16_t)(p.x & 0xFFFFu);
+          *(uint16_t*)(base + tile_lds_byte(vl + 1, tl)) = (uint16_t)(p.x >> 16);
+          *(uint16_t*)(base + tile_lds_byte(vl + 2, tl)) = (uint16_t)(p.y & 0xFFFFu);
+          *(uint16_t*)(base + tile_lds_byte(vl + 3, tl)) = (uint16_t)(p.y >> 16);
+        }
+    __syncthreads();
+    store_tile_blocked<G::NT>(lds, Gs, (uint32_t)n0 >> 6, Vc, (uint32_t)m0);
   }
 }
 
