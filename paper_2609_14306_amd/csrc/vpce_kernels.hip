@@ -136,6 +136,8 @@ struct Gemm {
   __device__ __forceinline__ static int wave_n(int wave) { return (wave % WGN) * WN; }
 
   // Row-major operands only (the k-block strides are for the direct-load tile).
+  // RAGGED is accepted for the interface of GemmDma and changes nothing here.
+  template <bool RAGGED = false>
   __device__ __forceinline__ static void run(f32x16_t (&acc)[MB][NB], const S* __restrict__ A,
                                              int64_t lda, int m0, int M, const S* __restrict__ B,
                                              int64_t ldb, int n0, int N, int K, S* smem,
@@ -378,7 +380,11 @@ struct GemmDma {
   // acc += A[m0 : m0+BM, 0:K] B[n0 : n0+BN, 0:K]^T; requires m0 < M and n0 < N.
   // Element (r, k) of A is at A[(k / 64) kblka + r lda + k % 64] (row-major:
   // kblka = 64; k-blocked: lda = 64, kblka = rows * 64), likewise for B.
+  // RAGGED: the tile reaches past row M of A; each wave skips the MFMAs (and the
+  // fragment reads) of its 32-row blocks of A that lie wholly at or past M, whose
+  // accumulators stay zero and are never stored.
   // LDS is free again for the caller when run() returns.
+  template <bool RAGGED = false>
   __device__ __forceinline__ static void run(f32x16_t (&acc)[MB][NB], const S* __restrict__ A,
                                              int64_t lda, int m0, int M, const S* __restrict__ B,
                                              int64_t ldb, int n0, int N, int K, S* smem,
@@ -389,6 +395,8 @@ struct GemmDma {
     const int wm = wave_m(wave), wn = wave_n(wave);
     const int nk = K / BK;
     if (nk <= 0) return;
+    // row blocks of A with live rows (wave-uniform); MB unless RAGGED
+    const int mb_live = RAGGED ? max(0, min(MB, (M - m0 - wm + 31) / 32)) : MB;
     const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) S*)smem;
     Loads L;
     plan(L, A, lda, m0, M, B, ldb, n0, N, wave, lane);
@@ -446,9 +454,10 @@ struct GemmDma {
 #pragma unroll
         for (int idx = 0; idx < NM; ++idx) {
           const int i = idx / NB, j = idx % NB;
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cur][i], b[cur][j], acc[i][j], 0, 0, 0);
+          if (!RAGGED || i < mb_live)
+            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cur][i], b[cur][j], acc[i][j], 0, 0, 0);
           __builtin_amdgcn_sched_barrier(0);
-          if (idx < NR) {
+          if (idx < NR && (!RAGGED || idx >= MB || idx < mb_live)) {
             const bf16x8_t f = read_one(src, wm, wn, skk, lane, idx);
             if (idx < MB)
               a[cur ^ 1][idx] = f;
@@ -857,7 +866,7 @@ __global__ void count_bad_kernel(const int64_t* targets, int64_t T, int64_t V, i
 
 // One float32 output tile of C = (beta ? C : 0) + A B^T (a dH or a dW tile; N, the
 // hidden width, is a multiple of 4).
-template <class E, class G>
+template <class E, class G, bool RAGGED = false>
 __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int nt,
                                           typename E::storage* smem) {
   using S = typename E::storage;
@@ -873,8 +882,8 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int nt,
   for (int i = 0; i < MB; ++i)
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
-  G::run(acc, (const S*)a.B, a.ldb, n0, a.N, (const S*)a.A, a.lda, m0, a.M, a.K, smem, a.kblkb,
-         a.kblka);
+  G::template run<RAGGED>(acc, (const S*)a.B, a.ldb, n0, a.N, (const S*)a.A, a.lda, m0, a.M, a.K, smem,
+                          a.kblkb, a.kblka);
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int m = m0 + wn + 32 * j + (lane & 31);
@@ -916,20 +925,22 @@ __global__ void __launch_bounds__(GM::NT, GM::OCC)
   const int xcd = blockIdx.x % 8;
   int local = blockIdx.x / 8;
   int mt, nt;
-  if (local < sp.cnt[0][xcd]) {
-    const int n_n = (h.N + GM::BM - 1) / GM::BM, n_m = (h.M + GM::BN - 1) / GM::BN;
-    grouped_tile(sp.first[0][xcd] + local, n_m, n_n, 4, mt, nt);
-    gemm_tile<E, GM>(h, mt, nt, smem);
-    return;
+  // dH (kind 0) and dW (kind 1) tiles; a tile of the last column block that reaches
+  // past the hidden width d runs ragged: the waves' row blocks past d do no MFMA work.
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    const GemmArgs& a = k == 0 ? h : w;
+    if (local < sp.cnt[k][xcd]) {
+      const int n_n = (a.N + GM::BM - 1) / GM::BM, n_m = (a.M + GM::BN - 1) / GM::BN;
+      grouped_tile(sp.first[k][xcd] + local, n_m, n_n, 4, mt, nt);
+      if ((nt + 1) * GM::BM > a.N)
+        gemm_tile<E, GM, true>(a, mt, nt, smem);
+      else
+        gemm_tile<E, GM>(a, mt, nt, smem);
+      return;
+    }
+    local -= sp.cnt[k][xcd];
   }
-  local -= sp.cnt[0][xcd];
-  if (local < sp.cnt[1][xcd]) {
-    const int n_n = (w.N + GM::BM - 1) / GM::BM, n_m = (w.M + GM::BN - 1) / GM::BN;
-    grouped_tile(sp.first[1][xcd] + local, n_m, n_n, 4, mt, nt);
-    gemm_tile<E, GM>(w, mt, nt, smem);
-    return;
-  }
-  local -= sp.cnt[1][xcd];
   const int n_tb = (g.N + GL::BN - 1) / GL::BN;
   grouped_tile(sp.first[2][xcd] + local, g.n_vt, n_tb, 4, mt, nt);
   grad_tile<E, GL>(g, mt, nt, smem);
