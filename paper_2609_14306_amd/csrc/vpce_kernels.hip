@@ -947,13 +947,16 @@ __global__ void __launch_bounds__(GM::NT, GM::OCC)
 }
 
 // out[c][r] = in[r][c] through a 64 x 64 LDS tile; rows R..R_pad-1 of the
-// output's columns are zero-filled.
+// output's columns are zero-filled.  One-dimensional grid of row-block-fastest
+// 64 x 64 tiles (either side alone can exceed 65535 blocks: T / 64 up to 2^17,
+// d / 64 up to 2^16).
 template <class S>
 __global__ void __launch_bounds__(256) transpose_kernel(TransposeArgs a) {
   __shared__ S tile[64][65];
   const S* in = (const S*)a.in;
   S* out = (S*)a.out;
-  const int r0 = blockIdx.x * 64, c0 = blockIdx.y * 64;
+  const uint32_t n_rb = ((uint32_t)a.R_pad + 63u) / 64u;
+  const int r0 = (int)(blockIdx.x % n_rb) * 64, c0 = (int)(blockIdx.x / n_rb) * 64;
   const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
   for (int i = ty; i < 64; i += 4) {
     const int r = r0 + i, c = c0 + tx;
@@ -1139,7 +1142,9 @@ bool run_bwd_stage(int dtype, const GemmArgs& h, const GemmArgs& w, const GradAr
 }
 bool run_transpose(int dtype, const TransposeArgs& a, hipStream_t s) {
   if (a.C <= 0 || a.R_pad <= 0) return true;
-  const dim3 grid((unsigned)((a.R_pad + 63) / 64), (unsigned)((a.C + 63) / 64));
+  const int64_t blocks = (int64_t)((a.R_pad + 63) / 64) * ((a.C + 63) / 64);
+  if (blocks > 0x7fffffff) return false;  // beyond any operand that fits in memory
+  const dim3 grid((unsigned)blocks);
   if (dtype == 1)
     hipLaunchKernelGGL(transpose_kernel<uint16_t>, grid, dim3(256), 0, s, a);
   else
