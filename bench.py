@@ -43,7 +43,87 @@ def parse():
     ap.add_argument("--strip-elems", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
                     help="only run one device-to-device copy of BYTES (for scaling HBM counters)")
+    ap.add_argument("--standard", action="store_true",
+                    help="instead of the bench line, compare the fused path with the dense standard "
+                         "(full logits, float32 log-softmax cross-entropy, autograd) on the same "
+                         "workload: time and peak memory above the resident tensors")
     return ap.parse_args()
+
+
+def standard_vs_fused(inp, H, Ws, tg, steps: int, warmup: int):
+    """The paper's comparison (its standard vs Ring-DTP table of peak memory and latency) on
+    one GPU: the dense standard materialises the [T, V] logits (bf16 product, as torch
+    computes it), takes a float32 log-softmax cross-entropy and backpropagates with autograd;
+    the fused path is this library's forward + backward.  Both start from the same resident
+    H, W and targets; memory is the peak allocation above them during a step.  The dense
+    path is plain torch, a baseline beside the product, not part of it."""
+    import torch
+    import torch.nn.functional as F
+
+    import paper_2609_14306_amd as vp
+
+    dev = H.device
+    T, d, V = inp.T, inp.d, inp.V
+    W = torch.cat(Ws, dim=0)  # vocabulary-id order
+    n_valid = int((inp.targets != inp.ignore_index).sum())
+    out = {}
+
+    def timed(step, pre=None):
+        for _ in range(warmup):
+            step()
+        torch.cuda.synchronize()
+        if pre is not None:
+            pre()
+        base = torch.cuda.memory_allocated()
+        torch.cuda.reset_peak_memory_stats()
+        e0 = torch.cuda.Event(enable_timing=True)
+        e1 = torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(steps):
+            step()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / steps, (torch.cuda.max_memory_allocated() - base) / 2**20
+
+    # dense standard; its H / W gradients are allocated by autograd inside the step
+    Hs = H.detach().clone().requires_grad_(True)
+    Wsd = W.detach().clone().requires_grad_(True)
+
+    def dense_step():
+        Hs.grad = None
+        Wsd.grad = None
+        logits = Hs @ Wsd.t()
+        loss = F.cross_entropy(logits.float(), tg, ignore_index=inp.ignore_index, reduction="mean")
+        loss.backward()
+
+    ms, mib = timed(dense_step, pre=lambda: (setattr(Hs, "grad", None), setattr(Wsd, "grad", None)))
+    out["standard"] = {"ms_per_step": ms, "peak_above_resident_mib": mib,
+                       "what": "logits = H W^T (bf16, [T, V] materialised), cross_entropy(logits.float()), "
+                               "autograd backward; includes the dH / dW outputs"}
+    del Hs, Wsd
+    torch.cuda.empty_cache()
+
+    # fused path; dH / dW outputs allocated inside the step like the dense one's gradients
+    prob = vp.problem_for(H, Ws, inp.ignore_index, inp.order)
+    fwd_b, bwd_b = vp.vp_ce_workspace_size(prob)
+    g = torch.full((T,), 1.0 / max(n_valid, 1), dtype=torch.float32, device=dev)
+
+    def fused_step():
+        ws = torch.empty(max(fwd_b, bwd_b), dtype=torch.uint8, device=dev)
+        loss = torch.empty(T, dtype=torch.float32, device=dev)
+        lse = torch.empty(T, dtype=torch.float32, device=dev)
+        vp.vp_ce_forward(prob, H, Ws, tg, loss, lse, ws)
+        dH = torch.empty(T, d, dtype=torch.float32, device=dev)
+        dWs = [torch.empty(x.shape[0], d, dtype=torch.float32, device=dev) for x in Ws]
+        vp.vp_ce_backward(prob, H, Ws, tg, lse, g, dH, dWs, ws)
+
+    ms, mib = timed(fused_step)
+    out["fused"] = {"ms_per_step": ms, "peak_above_resident_mib": mib,
+                    "what": "vp_ce_forward + vp_ce_backward; workspace, loss / lse and the dH / dW "
+                            "outputs allocated inside the step"}
+    out["outputs_mib"] = (T * d * 4 + V * d * 4) / 2**20
+    out["dense_logits_fp32_mib"] = T * V * 4 / 2**20
+    return out
 
 
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_14306_amd", "csrc", "vpce_kernels.hip")
@@ -125,6 +205,9 @@ def main():
         print(json.dumps({"copy_bytes": n * 4}), flush=True)
         return
     w = wl.WORKLOADS[args.workload]
+    if args.standard and w.dtype != "bf16":
+        print(json.dumps({"error": "--standard compares bf16 workloads"}))
+        sys.exit(2)
     t_gen = time.perf_counter()
     inp = wl.make_inputs(w)
     t_gen = time.perf_counter() - t_gen
@@ -138,6 +221,12 @@ def main():
     Ws = [to_dev(x) for x in inp.W_shards]
     tg = torch.from_numpy(inp.targets).to(dev)
     T, d, V = inp.T, inp.d, inp.V
+    if args.standard:
+        res = standard_vs_fused(inp, H, Ws, tg, args.steps, args.warmup)
+        res.update({"mode": "standard_vs_fused", "workload": w.name, "T": T, "d": d, "V": V,
+                    "steps": args.steps, "warmup": args.warmup})
+        print(json.dumps(res), flush=True)
+        return
     n_valid = int((inp.targets != inp.ignore_index).sum())
     g = torch.full((T,), 1.0 / max(n_valid, 1), dtype=torch.float32, device=dev)
     prob = vp.problem_for(H, Ws, inp.ignore_index, inp.order, 0, args.strip_elems)
