@@ -402,12 +402,12 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
   void* Ht = wsb + plan.off_ht;
   void* Wt = wsb + plan.off_wt;
   const size_t eb = elem_bytes(prob->dtype);
-  // bfloat16 workspaces (the residual strips, H^T and W^T) are k-blocked: every
-  // 64-deep slice of a 256-row tile the dH / dW contractions stream is one
-  // contiguous 32 KiB block; float32 ones are row-major.
-  const int32_t blocked = prob->dtype == VP_BF16 ? 1 : 0;
+  // The workspaces (the residual strips, H^T and W^T) are k-blocked in 128-byte
+  // blocks of KB elements (64 bfloat16, 32 float32): every k-slice of a 256-row
+  // tile the dH / dW contractions stream is one contiguous 32 KiB block.
+  const int64_t KB = ts.kblock;
 
-  {  // H^T [d][T_pad] (k-blocked: [T_pad/64][d][64]), zero beyond T
+  {  // H^T [d][T_pad], k-blocked: [T_pad/KB][d][KB], zero beyond T
     vpce::TransposeArgs tr;
     tr.in = H;
     tr.ld_in = d;
@@ -416,7 +416,7 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
     tr.R = (int32_t)T;
     tr.C = (int32_t)d;
     tr.R_pad = (int32_t)plan.T_pad;
-    tr.blocked = blocked;
+    tr.blocked = 1;
     if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
   }
 
@@ -463,7 +463,7 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
     memset(&w, 0, sizeof(w));
     if (k >= 1) {
       const Chunk& c = chunks[k - 1];
-      if (c.new_vchunk) {  // W^T of this vocabulary chunk, [d][Vc], zero beyond M
+      if (c.new_vchunk) {  // W^T of this vocabulary chunk, k-blocked [Vc/KB][d][KB], zero beyond M
         vpce::TransposeArgs tr;
         tr.in = wchunk(c);
         tr.ld_in = d;
@@ -471,17 +471,17 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
         tr.ld_out = plan.Vc;
         tr.R = (int32_t)c.M;
         tr.C = (int32_t)d;
-        tr.R_pad = (int32_t)round_up(c.M, 64);  // >= the K the dH launch reads
-        tr.blocked = blocked;
+        tr.R_pad = (int32_t)round_up(c.M, KB);  // >= the K the dH launch reads
+        tr.blocked = 1;
         if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
       }
       // dH[t0 : t0+N] (+)= G^T W_chunk = G^T . (W^T)^T
       h.A = wsb + plan.off_gt[(k - 1) % 2];
-      h.lda = blocked ? 64 : plan.Vc;
-      h.kblka = blocked ? plan.Tc * 64 : 64;
+      h.lda = KB;
+      h.kblka = plan.Tc * KB;
       h.B = Wt;
-      h.ldb = blocked ? 64 : plan.Vc;
-      h.kblkb = blocked ? d * 64 : 64;
+      h.ldb = KB;
+      h.kblkb = d * KB;
       h.C = dH + c.t0 * d;
       h.ldc = d;
       h.M = (int32_t)c.N;
@@ -490,11 +490,11 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
       h.beta = c.first_vchunk ? 0 : 1;
       // dW_chunk (+)= G H[t0 : t0+N] = G . (H^T)^T
       w.A = wsb + plan.off_g[(k - 1) % 2];
-      w.lda = blocked ? 64 : plan.Tc;
-      w.kblka = blocked ? plan.Vc * 64 : 64;
-      w.B = (const char*)Ht + (size_t)(blocked ? (c.t0 / 64) * d * 64 : c.t0) * eb;
-      w.ldb = blocked ? 64 : plan.T_pad;
-      w.kblkb = blocked ? d * 64 : 64;
+      w.lda = KB;
+      w.kblka = plan.Vc * KB;
+      w.B = (const char*)Ht + (size_t)((c.t0 / KB) * d * KB) * eb;  // t0 is a multiple of Tc
+      w.ldb = KB;
+      w.kblkb = d * KB;
       w.C = dW_shards[c.q] + c.v0 * d;
       w.ldc = d;
       w.M = (int32_t)c.M;

@@ -68,12 +68,11 @@ struct GradArgs {
   const int64_t* targets;
   const float* lse;
   const float* grad;
-  // The residual strip in two layouts, Tc tokens by Vc vocabulary rows each:
-  //   float32: G [Vc][Tc] and G^T [Tc][Vc], row-major;
-  //   bfloat16: k-blocked, G [Tc/64][Vc][64] (element (v, t) at
-  //   ((t / 64) Vc + v) 64 + t % 64) and G^T [Vc/64][Tc][64] (element (t, v) at
-  //   ((v / 64) Tc + t) 64 + v % 64), so that a 64-deep slice of a 256-row tile
-  //   of either operand is one contiguous 32 KiB block.
+  // The residual strip in two layouts, Tc tokens by Vc vocabulary rows each,
+  // k-blocked in 128-byte blocks of KB elements (64 bfloat16, 32 float32):
+  // G [Tc/KB][Vc][KB] (element (v, t) at ((t / KB) Vc + v) KB + t % KB) and
+  // G^T [Vc/KB][Tc][KB] (element (t, v) at ((v / KB) Tc + t) KB + v % KB), so that a
+  // KB-deep slice of a 256-row tile of either operand is one contiguous 32 KiB block.
   void* strip;
   void* strip_t;
   int64_t Tc, Vc;
@@ -97,15 +96,16 @@ struct GemmArgs {
   int64_t ldc;
   int32_t M, N, K;
   int32_t beta;
-  // elements between consecutive 64-wide k blocks of A and of B: 64 for a
-  // row-major operand, rows * 64 for a k-blocked one (whose row pitch is 64)
+  // elements between consecutive k-blocks (KB = 64 bfloat16 or 32 float32 wide)
+  // of A and of B: KB for a row-major operand, rows * KB for a k-blocked one
+  // (whose row pitch is KB)
   int64_t kblka, kblkb;
 };
 
-// out[c][r] = in[r][c] for r < R, c < C; out[c][r] = 0 for R <= r < R_pad.
 // out[c][r] = in[r][c] for r < R (zero for R <= r < R_pad), c < C.  blocked == 0:
-// out is row-major with pitch ld_out; blocked != 0: out is k-blocked,
-// [R_pad/64][C][64] (element (c, r) at ((r / 64) C + c) 64 + r % 64).
+// out is row-major with pitch ld_out; blocked != 0: out is k-blocked in 128-byte
+// blocks of KB elements (64 bfloat16, 32 float32), [R_pad/KB][C][KB] (element
+// (c, r) at ((r / KB) C + c) KB + r % KB).
 struct TransposeArgs {
   const void* in;
   int64_t ld_in;
@@ -118,6 +118,7 @@ struct TransposeArgs {
 struct TileShape {
   int fwd_bm, fwd_bn, grad_bm, grad_bn;
   int kalign;  // the dH / dW contractions are launched with K rounded up to this
+  int kblock;  // elements of one 128-byte k-block of the backward workspaces
 };
 
 TileShape tile_shape(int dtype);

@@ -35,11 +35,18 @@ constexpr float kLn2 = 0.6931471805599453f;
 // ---------------------------------------------------------------------------
 // Element policies.  BK: k elements staged per LDS pass (128 bytes per row);
 // KSTEP: k consumed by one MFMA; VEC: elements per 16 bytes.
+// KB: elements of one 128-byte k-block of the k-blocked backward workspaces (and of
+// one row of a direct-to-LDS slice).  frag16 / mma16: one 16-byte operand fragment
+// per lane (8 bfloat16 or 4 float32 k values) and the MFMA work it feeds.
 struct Bf16 {
   using storage = uint16_t;
   using frag = bf16x8_t;
-  static constexpr int BK = 64, KSTEP = 16, VEC = 8, PADK = 8;
+  using frag16 = bf16x8_t;
+  static constexpr int BK = 64, KSTEP = 16, VEC = 8, PADK = 8, KB = 64;
   __device__ static f32x16_t mma(frag a, frag b, f32x16_t c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+  __device__ static f32x16_t mma16(frag16 a, frag16 b, f32x16_t c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
   __device__ static storage from_f32(float x) {  // round to nearest even (NaN stays NaN)
@@ -48,12 +55,23 @@ struct Bf16 {
     return (storage)(u >> 16);
   }
 };
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 struct F32 {
   using storage = float;
   using frag = float;
-  static constexpr int BK = 32, KSTEP = 2, VEC = 4, PADK = 4;
+  using frag16 = f32x4_t;
+  static constexpr int BK = 32, KSTEP = 2, VEC = 4, PADK = 4, KB = 32;
   __device__ static f32x16_t mma(frag a, frag b, f32x16_t c) {
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  // Lane half h holds k = 4h .. 4h + 3 of an 8-wide k group in both operands; MFMA q
+  // takes element q, i.e. k = q (lanes 0-31) and 4 + q (lanes 32-63): the four MFMAs
+  // together cover the group (the contraction order within it is a permutation).
+  __device__ static f32x16_t mma16(frag16 a, frag16 b, f32x16_t c) {
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[0], b[0], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[1], b[1], c, 0, 0, 0);
+    c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[2], b[2], c, 0, 0, 0);
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a[3], b[3], c, 0, 0, 0);
   }
   __device__ static storage from_f32(float x) { return x; }
 };
@@ -194,10 +212,13 @@ struct Gemm {
 };
 
 // ---------------------------------------------------------------------------
-// bf16 tile GEMM fed by direct global -> LDS loads (global_load_lds_dwordx4,
-// 16 bytes per lane straight into LDS, no staging registers) through a ring of
-// two k-slices of BK = 64.  Requires K to be a multiple of 64 and both operands
-// to hold finite values up to that K (the backward's buffers are zero-padded).
+// Tile GEMM fed by direct global -> LDS loads (global_load_lds_dwordx4, 16 bytes
+// per lane straight into LDS, no staging registers) through a ring of two
+// k-slices of 128-byte rows: 64 bfloat16 or 32 float32 k values per row.  A
+// 16-byte fragment feeds one 32x32x16 bf16 MFMA or four 32x32x2 f32 MFMAs (see
+// the element policies); everything else is the same for both types.  Requires K
+// to be a multiple of the slice depth and both operands to hold finite values up
+// to that K (the backward's buffers are zero-padded).
 //
 // LDS slice layout: the A rows then the B rows, 128 bytes (eight 16-byte
 // chunks) per row, chunk c of row r stored in slot c ^ ((r >> 1) & 7): the 16
@@ -224,28 +245,6 @@ struct Gemm {
 // which ring slot a read touches) nor keeps 64-bit addresses per load.
 // Completion is tracked by hand with vmcnt: loads return in issue order and the
 // only loads a wave has in flight are its slice loads.
-// Four loads from one scalar base into four LDS destinations, as one asm block
-// so that nothing the compiler schedules can land between them.  The hazards
-// the compiler's hazard recognizer cannot see inside inline assembly are
-// covered here: five wait states before the first load in case a VALU
-// instruction (v_readlane of a spilled value, a carry-out) wrote the base
-// SGPRs just before the block, and one after each M0 write, which an LDS DMA
-// reads.
-__device__ __forceinline__ void lds_dma16x4(const void* sbase, uint32_t o0, uint32_t o1,
-                                            uint32_t o2, uint32_t o3, uint32_t l0, uint32_t l1,
-                                            uint32_t l2, uint32_t l3) {
-  uint32_t m0v = l0;  // M0 is an operand (not a clobber): the compiler knows the block writes it
-  asm volatile(
-      "s_nop 4\n\t"
-      "s_nop 0\n\tglobal_load_lds_dwordx4 %1, %5\n\t"
-      "s_mov_b32 m0, %6\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %2, %5\n\t"
-      "s_mov_b32 m0, %7\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %3, %5\n\t"
-      "s_mov_b32 m0, %8\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %4, %5"
-      : "+{m0}"(m0v)
-      : "v"(o0), "v"(o1), "v"(o2), "v"(o3), "s"(sbase), "s"(l1), "s"(l2), "s"(l3)
-      : "memory");
-}
-
 template <int N>
 __device__ __forceinline__ void wait_vmcnt() {
   static_assert(N >= 0 && N < 64, "vmcnt range");
@@ -254,7 +253,11 @@ __device__ __forceinline__ void wait_vmcnt() {
 }
 __device__ __forceinline__ void wait_lgkmcnt0() { __builtin_amdgcn_s_waitcnt(0xC07F); }
 
-// One load on its own, with the same wait states.
+// One direct-to-LDS load from a scalar base.  The hazards the compiler's hazard
+// recognizer cannot see inside inline assembly are covered here: five wait states
+// before the load in case a VALU instruction (v_readlane of a spilled value, a
+// carry-out) wrote the base SGPRs just before it, and one after the M0 write,
+// which an LDS DMA reads.
 __device__ __forceinline__ void lds_dma16x1(const void* sbase, uint32_t o0, uint32_t l0) {
   uint32_t m0v = l0;
   asm volatile("s_nop 4\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2"
@@ -263,9 +266,10 @@ __device__ __forceinline__ void lds_dma16x1(const void* sbase, uint32_t o0, uint
                : "memory");
 }
 
-template <int BM_, int BN_, int WGM_, int WGN_, int BK_ = 64, int STAGES_ = 2>
+template <int BM_, int BN_, int WGM_, int WGN_, int BK_ = 64, int STAGES_ = 2, class E = Bf16>
 struct GemmDma {
-  using S = uint16_t;
+  using S = typename E::storage;
+  using F16 = typename E::frag16;
   static constexpr int BM = BM_, BN = BN_, WGM = WGM_, WGN = WGN_;
   static constexpr int NT = 64 * WGM * WGN, NWAVES = WGM * WGN;
   // One workgroup per CU (the ring takes 128 to 160 KiB of LDS): 512 threads run
@@ -273,13 +277,16 @@ struct GemmDma {
   static constexpr int OCC = 1;
   static constexpr int WM = BM / WGM, WN = BN / WGN, MB = WM / 32, NB = WN / 32;
   static_assert(WM % 32 == 0 && WN % 32 == 0, "wave tile must be whole 32x32 blocks");
-  static constexpr int BK = BK_, STAGES = STAGES_;
-  static_assert((BK == 32 || BK == 64) && STAGES >= 2, "slice depth and ring slots");
+  // BK_ sizes a slice row in bfloat16 units: 64 (128-byte rows) or 32 (64-byte rows)
+  static constexpr int STAGES = STAGES_;
+  static constexpr int ROW_BYTES = BK_ * 2;
+  static constexpr int BK = ROW_BYTES / (int)sizeof(S);  // k values per slice
+  static_assert((BK_ == 32 || BK_ == 64) && STAGES >= 2, "slice depth and ring slots");
+  static_assert(E::KB % BK == 0, "slices never straddle a k-block of the layout");
   static constexpr int KDIV = BK;                 // K must be a multiple of the slice depth
-  static constexpr int NKK = BK / 16;             // MFMA sub-steps per slice
+  static constexpr int NKK = ROW_BYTES / 32;      // sub-steps per slice (two 16-byte chunks each)
   static_assert(NKK % 2 == 0, "register sets alternate per sub-step across slices");
-  static constexpr int CPR = BK / 8;              // 16-byte chunks per row
-  static constexpr int ROW_BYTES = BK * 2;
+  static constexpr int CPR = ROW_BYTES / 16;      // 16-byte chunks per row
   static constexpr int RPW = 256 / ROW_BYTES;     // rows per 64-bank (256-byte) window
   static constexpr int RPI = 1024 / ROW_BYTES;    // rows per 1 KiB load instruction
   static constexpr int SLICE_BYTES = (BM + BN) * ROW_BYTES;
@@ -290,8 +297,8 @@ struct GemmDma {
   static_assert(NLOADS % 2 == 0, "loads go out in two halves");
   static constexpr int NM = MB * NB, NR = MB + NB;   // MFMAs and fragment reads per sub-step
   static_assert(NR <= NM && NLOADS / 2 <= (NM + 1) / 2, "interleave slots");
-  static constexpr int LDS_ELEMS = STAGES * SLICE_BYTES / 2;
-  static_assert(LDS_ELEMS * 2 <= 160 * 1024, "LDS");
+  static constexpr int LDS_ELEMS = STAGES * SLICE_BYTES / (int)sizeof(S);
+  static_assert(STAGES * SLICE_BYTES <= 160 * 1024, "LDS");
 
   // Chunk c of slice row r lives in slot c ^ key(r): within one 256-byte window
   // the rows sit at distinct offsets, and key(r) differs for the CPR rows that
@@ -313,7 +320,7 @@ struct GemmDma {
   struct Loads {
     const char* baseA;  // byte address of the tile's first A row (k = 0)
     const char* baseB;
-    int64_t kblkA, kblkB;  // elements between consecutive 64-wide k blocks
+    int64_t kblkA, kblkB;  // elements between consecutive k-blocks (E::KB wide)
     uint32_t offA[A_LOADS], offB[B_LOADS];  // per-lane byte offsets from the bases
   };
 
@@ -328,13 +335,13 @@ struct GemmDma {
     for (int q = 0; q < A_LOADS; ++q) {
       const int r = (wave + q * NWAVES) * RPI + row_in;
       const int c = (lane % CPR) ^ key(r);
-      L.offA[q] = (uint32_t)((min(m0 + r, M - 1) - ma) * lda * 2) + 16u * c;
+      L.offA[q] = (uint32_t)((min(m0 + r, M - 1) - ma) * lda * (int64_t)sizeof(S)) + 16u * c;
     }
 #pragma unroll
     for (int q = 0; q < B_LOADS; ++q) {
       const int r = (wave + (A_LOADS + q) * NWAVES) * RPI + row_in;  // >= BM
       const int c = (lane % CPR) ^ key(r);
-      L.offB[q] = (uint32_t)((min(n0 + r - BM, N - 1) - nb) * ldb * 2) + 16u * c;
+      L.offB[q] = (uint32_t)((min(n0 + r - BM, N - 1) - nb) * ldb * (int64_t)sizeof(S)) + 16u * c;
     }
   }
 
@@ -342,22 +349,23 @@ struct GemmDma {
   // it fills the 1 KiB at (wave + q * NWAVES) KiB of the slot.
   __device__ __forceinline__ static void issue_one(const Loads& L, int kt, int q, uint32_t lds0,
                                                    int wave) {
+    constexpr int KB = E::KB;
     const int64_t k0 = (int64_t)kt * BK;
     const uint32_t l = lds0 + slot_bytes(kt) + (uint32_t)(wave * 1024) + q * NWAVES * 1024;
     if (q < A_LOADS)
-      lds_dma16x1(L.baseA + ((k0 >> 6) * L.kblkA + (k0 & 63)) * 2, L.offA[q], l);
+      lds_dma16x1(L.baseA + ((k0 / KB) * L.kblkA + (k0 % KB)) * (int64_t)sizeof(S), L.offA[q], l);
     else
-      lds_dma16x1(L.baseB + ((k0 >> 6) * L.kblkB + (k0 & 63)) * 2, L.offB[q - A_LOADS], l);
+      lds_dma16x1(L.baseB + ((k0 / KB) * L.kblkB + (k0 % KB)) * (int64_t)sizeof(S), L.offB[q - A_LOADS], l);
   }
 
-  // Fragment idx (the MB A blocks, then the NB B blocks) of sub-step kk at `slot`:
-  // lane l takes row l % 32 of the block and k = 16 kk + 8 (l / 32) + 0..7, i.e.
-  // chunk 2 kk + l / 32.
-  __device__ __forceinline__ static bf16x8_t read_one(const S* slot, int wm, int wn, int kk,
-                                                      int lane, int idx) {
+  // Fragment idx (the MB A blocks, then the NB B blocks) of sub-step kk at slot
+  // byte address `slot`: lane l takes row l % 32 of the block and the 16 bytes of
+  // chunk 2 kk + l / 32 (bf16: k = 16 kk + 8 (l / 32) + 0..7).
+  __device__ __forceinline__ static F16 read_one(const char* slot, int wm, int wn, int kk, int lane,
+                                                 int idx) {
     const int chunk = 2 * kk + (lane >> 5);
     const int row = idx < MB ? wm + 32 * idx + (lane & 31) : BM + wn + 32 * (idx - MB) + (lane & 31);
-    return *(const bf16x8_t*)(slot + row * BK + ((chunk ^ key(row)) << 3));
+    return *(const F16*)(slot + row * ROW_BYTES + ((chunk ^ key(row)) << 4));
   }
 
   // Wait until at most n slices' loads (n in [0, STAGES - 1]) of this wave are in
@@ -378,8 +386,8 @@ struct GemmDma {
   }
 
   // acc += A[m0 : m0+BM, 0:K] B[n0 : n0+BN, 0:K]^T; requires m0 < M and n0 < N.
-  // Element (r, k) of A is at A[(k / 64) kblka + r lda + k % 64] (row-major:
-  // kblka = 64; k-blocked: lda = 64, kblka = rows * 64), likewise for B.
+  // Element (r, k) of A is at A[(k / KB) kblka + r lda + k % KB] with KB = E::KB
+  // (row-major: kblka = KB; k-blocked: lda = KB, kblka = rows * KB), likewise for B.
   // RAGGED: the tile reaches past row M of A; each wave skips the MFMAs (and the
   // fragment reads) of its 32-row blocks of A that lie wholly at or past M, whose
   // accumulators stay zero and are never stored.
@@ -388,7 +396,7 @@ struct GemmDma {
   __device__ __forceinline__ static void run(f32x16_t (&acc)[MB][NB], const S* __restrict__ A,
                                              int64_t lda, int m0, int M, const S* __restrict__ B,
                                              int64_t ldb, int n0, int N, int K, S* smem,
-                                             int64_t kblka = 64, int64_t kblkb = 64) {
+                                             int64_t kblka = E::KB, int64_t kblkb = E::KB) {
     // The wave index is made scalar so that every branch on it is a scalar branch.
     const int tid = threadIdx.x, lane = tid & 63;
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -409,10 +417,11 @@ struct GemmDma {
       for (int q = 0; q < NLOADS; ++q) issue_one(L, kt, q, lds0, wave);
     wait_slices(pro - 1);
     __builtin_amdgcn_s_barrier();
-    bf16x8_t a[2][MB], b[2][NB];
+    const char* ring = (const char*)smem;
+    F16 a[2][MB], b[2][NB];
 #pragma unroll
     for (int idx = 0; idx < NR; ++idx) {
-      const bf16x8_t f = read_one(smem, wm, wn, 0, lane, idx);
+      const F16 f = read_one(ring, wm, wn, 0, lane, idx);
       if (idx < MB)
         a[0][idx] = f;
       else
@@ -423,10 +432,10 @@ struct GemmDma {
       for (int kk = 0; kk < NKK; ++kk) {
         const int cur = kk & 1;
         // where the fragments of the next sub-step come from
-        const S* src;
+        const char* src;
         int skk;
         if (kk + 1 < NKK) {
-          src = smem + slot_bytes(kt) / 2;
+          src = ring + slot_bytes(kt);
           skk = kk + 1;
         } else {
           // Slice kt+1 must have landed; slices kt+2 .. kt+STAGES-1 may still be
@@ -436,7 +445,7 @@ struct GemmDma {
           wait_slices(min(STAGES - 2, nk - 2 - kt));
           wait_lgkmcnt0();  // this wave's reads of slice kt
           __builtin_amdgcn_s_barrier();
-          src = smem + slot_bytes(kt + 1) / 2;
+          src = ring + slot_bytes(kt + 1);
           skk = 0;
         }
         // The loads of slice kt+STAGES go out in two halves: the first during the
@@ -454,11 +463,10 @@ struct GemmDma {
 #pragma unroll
         for (int idx = 0; idx < NM; ++idx) {
           const int i = idx / NB, j = idx % NB;
-          if (!RAGGED || i < mb_live)
-            acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[cur][i], b[cur][j], acc[i][j], 0, 0, 0);
+          if (!RAGGED || i < mb_live) acc[i][j] = E::mma16(a[cur][i], b[cur][j], acc[i][j]);
           __builtin_amdgcn_sched_barrier(0);
           if (idx < NR && (!RAGGED || idx >= MB || idx < mb_live)) {
-            const bf16x8_t f = read_one(src, wm, wn, skk, lane, idx);
+            const F16 f = read_one(src, wm, wn, skk, lane, idx);
             if (idx < MB)
               a[cur ^ 1][idx] = f;
             else
@@ -764,8 +772,9 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
   G::run(acc, (const S*)a.W, a.d, m0, a.M, (const S*)a.H + a.t0 * a.d, a.d, n0, a.N, a.d, smem);
 
   // Strip offsets fit in 32 bits (the strip budget is capped below 2^31 elements).
-  // bfloat16 strips are k-blocked, float32 strips row-major (see GradArgs).
-  constexpr bool kBlocked = sizeof(S) == 2;
+  // Both strips are k-blocked (see GradArgs) with KB = E::KB elements per block.
+  constexpr bool kBlocked = sizeof(S) == 2;  // bfloat16 tiles are staged through LDS
+  constexpr uint32_t KB = E::KB;
   S* __restrict__ Gs = (S*)a.strip;
   S* __restrict__ Gt = (S*)a.strip_t;
   const uint32_t Tc = (uint32_t)a.Tc, Vc = (uint32_t)a.Vc;
@@ -808,13 +817,15 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r4 + q], kLog2e, -lse2));
           const float v = (live && ml < a.M) ? g * (p - (rel == ml ? 1.f : 0.f)) : 0.f;
           v4[q] = E::from_f32(v);
-          if constexpr (!kBlocked) Gs[(uint32_t)ml * Tc + (uint32_t)nl] = v4[q];
+          if constexpr (!kBlocked)
+            Gs[(((uint32_t)nl / KB) * Vc + (uint32_t)ml) * KB + (uint32_t)nl % KB] = v4[q];
         }
         if constexpr (kBlocked) {
           packed[j][i][r4 >> 2].x = (uint32_t)v4[0] | ((uint32_t)v4[1] << 16);
           packed[j][i][r4 >> 2].y = (uint32_t)v4[2] | ((uint32_t)v4[3] << 16);
-        } else {
-          *(float4*)(Gt + (uint32_t)nl * Vc + (uint32_t)ml0) = make_float4(v4[0], v4[1], v4[2], v4[3]);
+        } else {  // 4 consecutive vocabulary rows: one 16-byte store into a 32-wide k-block
+          *(float4*)(Gt + (((uint32_t)ml0 / KB) * Tc + (uint32_t)nl) * KB + (uint32_t)ml0 % KB) =
+              make_float4(v4[0], v4[1], v4[2], v4[3]);
         }
       }
   }
@@ -966,7 +977,8 @@ __global__ void __launch_bounds__(256) transpose_kernel(TransposeArgs a) {
   for (int i = ty; i < 64; i += 4) {
     const int c = c0 + i, r = r0 + tx;
     if (c < a.C && r < a.R_pad) {
-      const int64_t o = a.blocked ? ((int64_t)(r >> 6) * a.C + c) * 64 + (r & 63)
+      constexpr int KB = 128 / (int)sizeof(S);  // elements of a 128-byte k-block
+      const int64_t o = a.blocked ? ((int64_t)(r / KB) * a.C + c) * KB + (r % KB)
                                   : (int64_t)c * a.ld_out + r;
       out[o] = tile[tx][i];
     }
@@ -994,11 +1006,14 @@ template <> struct Cfg<Bf16> {
   static constexpr int KALIGN = 64;  // K granularity the dH / dW launches need
 };
 template <> struct Cfg<F32> {
-  using Logits = Gemm<F32, 64, 64, 2, 2>;
-  using LogitsReg = Logits;
-  using MmA = Gemm<F32, 64, 64, 2, 2>;
-  using MmB = Gemm<F32, 64, 64, 2, 2>;
-  static constexpr int KALIGN = 1;
+  // The same direct-to-LDS ring and 256 x 256 tiles: 32 float32 k values per slice,
+  // four 32x32x2 f32 MFMAs per fragment pair.  d not a multiple of 32: the
+  // register-staged tile of the same shape.
+  using Logits = GemmDma<256, 256, 2, 4, 64, 2, F32>;
+  using MmA = Logits;
+  using MmB = MmA;
+  using LogitsReg = Gemm<F32, Logits::BM, Logits::BN, Logits::WGM, Logits::WGN>;
+  static constexpr int KALIGN = 32;  // K granularity the dH / dW launches need
 };
 
 static inline bool launched_ok() { return hipGetLastError() == hipSuccess; }
@@ -1083,15 +1098,22 @@ TileShape tile_shape(int dtype) {
   static_assert(Cfg<Bf16>::Logits::BM == Cfg<Bf16>::LogitsReg::BM &&
                     Cfg<Bf16>::Logits::BN == Cfg<Bf16>::LogitsReg::BN,
                 "both logits mainloops must share the tile shape");
+  static_assert(Cfg<F32>::Logits::BM == Cfg<F32>::LogitsReg::BM &&
+                    Cfg<F32>::Logits::BN == Cfg<F32>::LogitsReg::BN,
+                "both logits mainloops must share the tile shape");
+  static_assert(Cfg<Bf16>::KALIGN == Bf16::KB && Cfg<F32>::KALIGN == F32::KB,
+                "dH / dW contractions read whole k-blocks");
   TileShape t;
   if (dtype == 1) {
     t.fwd_bm = t.grad_bm = Cfg<Bf16>::Logits::BM;
     t.fwd_bn = t.grad_bn = Cfg<Bf16>::Logits::BN;
     t.kalign = Cfg<Bf16>::KALIGN;
+    t.kblock = Bf16::KB;
   } else {
     t.fwd_bm = t.grad_bm = Cfg<F32>::Logits::BM;
     t.fwd_bn = t.grad_bn = Cfg<F32>::Logits::BN;
     t.kalign = Cfg<F32>::KALIGN;
+    t.kblock = F32::KB;
   }
   return t;
 }
