@@ -38,7 +38,8 @@ def parse():
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default=DEFAULT_WORKLOAD)
     ap.add_argument("--cpu-sample-rows", type=int, default=4096,
-                    help="token rows of the workload the CPU oracle is timed on")
+                    help="token rows of the workload the CPU oracle is timed on (at most; fewer "
+                         "when V * d is large, so that the sample stays near 20 s of host work)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--strip-elems", type=int, default=0)
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="BYTES",
@@ -166,7 +167,9 @@ def cpu_baseline(inp, rows: int):
         cores = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
     except Exception:  # noqa: BLE001
         cores = os.cpu_count() or 1
-    rows = min(rows, inp.T)
+    # about 1.6e13 float64 operations (6 T V d for the forward and backward products)
+    cap = max(256, int(1.6e13 / (6.0 * inp.V * inp.d)) // 256 * 256)
+    rows = min(rows, cap, inp.T)
     H = wl.to_f64(inp.H[:rows], inp.dtype)
     Ws = [wl.to_f64(w, inp.dtype) for w in inp.W_shards]
     g = wl.random_grad_loss(rows, 0, "sum")

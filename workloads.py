@@ -65,6 +65,11 @@ WORKLOADS = {
         # draws is ~6.47*h_scale, so 6.18 puts it near 40.
         Workload("stress_bf16_T65536_d4096_V151936_P16_rev", 65536, 4096, 151936, 16, "bf16", 0,
                  6.18, "zipf", 1.3, 0.10, "ring0_reversed"),
+        # The paper's own isolated vocabulary-projection benchmark (Sec. 3.2 table, App. C):
+        # one rank's share, N = 16384 local tokens, hidden 7168, V = 200000 over P = 8
+        # shards, FP32, move-weights ring order.
+        Workload("paper_f32_T16384_d7168_V200000_P8_ring", 16384, 7168, 200000, 8, "f32", 0, 1.0,
+                 "uniform", 0.0, 0.0, "ring0"),
     ]
 }
 WORKLOAD_LIST = list(WORKLOADS.values())
