@@ -129,6 +129,7 @@ def standard_vs_fused(inp, H, Ws, tg, steps: int, warmup: int):
 
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2609_14306_amd", "csrc", "vpce_kernels.hip")
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "hbm_traffic_longctx_T32768_d2880_V201088.md")
+MFMA_PROFILE = os.path.join(ROOT, "profiles", "mfma_util_longctx_T32768_d2880_V201088.md")
 
 
 def kernel_source_sha256() -> str:
@@ -137,22 +138,42 @@ def kernel_source_sha256() -> str:
         return hashlib.sha256(f.read()).hexdigest()
 
 
-def measured_traffic(kernel: str, workload: str):
-    """HBM bytes per launch of `kernel` from the committed counter profile, or None when the
-    profile is missing, covers another workload, or the kernels changed since it was taken."""
+def profile_values(path: str, workload: str) -> dict:
+    """The "- key: `value`" lines of a committed profile summary, or {} when the file is
+    missing, covers another workload, or the kernels changed since it was taken."""
     try:
-        lines = open(TRAFFIC_PROFILE).read().splitlines()
+        lines = open(path).read().splitlines()
     except OSError:
-        return None
+        return {}
     vals = {}
     for ln in lines:
         if ln.startswith("- ") and ":" in ln:
             k, v = ln[2:].split(":", 1)
             vals[k.strip()] = v.strip().strip("`")
     if vals.get("workload") != workload or vals.get("kernel_source_sha256") != kernel_source_sha256():
+        return {}
+    return vals
+
+
+def measured_traffic(kernel: str, workload: str):
+    """HBM bytes per launch of `kernel` from the committed counter profile, or None."""
+    v = profile_values(TRAFFIC_PROFILE, workload).get(f"{kernel}_hbm_bytes_per_launch")
+    return float(v) if v is not None else None
+
+
+def measured_clock(kernel: str, workload: str):
+    """Clock and MFMA occupancy of `kernel` from the committed counter profile, or None.
+
+    The nameplate MFMA peak assumes 2.4 GHz; `peak_at_clock` is the same peak at the clock the
+    counters saw the kernel hold (GRBM_GUI_ACTIVE per XCD over the dispatch duration)."""
+    vals = profile_values(MFMA_PROFILE, workload)
+    try:
+        ghz = float(vals[f"{kernel}_clock_ghz"])
+        busy = float(vals[f"{kernel}_mfma_busy"])
+    except (KeyError, ValueError):
         return None
-    key = f"{kernel}_hbm_bytes_per_launch"
-    return float(vals[key]) if key in vals else None
+    return {"clock_ghz": ghz, "mfma_busy": busy, "peak_at_clock": PEAK_BF16_TFLOPS * ghz / 2.4,
+            "source": os.path.relpath(MFMA_PROFILE, ROOT)}
 
 
 def cpu_baseline(inp, rows: int):
@@ -315,11 +336,13 @@ def main():
                      "launches_per_step": plan["stage_launches"],
                      "flops_per_launch": 6.0 * T * V * d / max(plan["stage_launches"], 1),
                      "avg_launch_ms": bwd_avg / max(plan["stage_launches"], 1),
-                     "strip": {"Tc": plan["Tc"], "Vc": plan["Vc"], "strips": plan["strips"]}},
+                     "strip": {"Tc": plan["Tc"], "Vc": plan["Vc"], "strips": plan["strips"]},
+                     "counters": measured_clock("bwd_stage_kernel", w.name)},
         "roofline_fwd": {"kernel": "fwd_kernel (fused logits tiles + online LSE fold)",
                          "bound": "mfma", "achieved": fwd_tflops, "peak": peak, "unit": "TFLOP/s",
                          "frac": fwd_tflops / peak, "traffic": fwd_traffic, "launches_per_step": 1,
-                         "flops_per_launch": 2.0 * T * V * d, "avg_launch_ms": fwd_avg},
+                         "flops_per_launch": 2.0 * T * V * d, "avg_launch_ms": fwd_avg,
+                         "counters": measured_clock("fwd_kernel", w.name)},
         "bad_targets": bad,
         "input_gen_s": t_gen,
     }
