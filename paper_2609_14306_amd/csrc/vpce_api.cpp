@@ -148,6 +148,35 @@ vp_status check_shards(const vp_problem* p, const void* const* W_shards) {
   return VP_OK;
 }
 
+// The strips of a backward call in visiting order: shards in `order`, each cut
+// into balanced, tile-aligned vocabulary chunks (never above Vc), each chunk
+// meeting every token chunk.
+struct Chunk {
+  int q;
+  int64_t v0, M, t0, N;
+  bool new_vchunk, first_vchunk;
+};
+
+std::vector<Chunk> strip_chunks(const vp_problem* prob, const StripPlan& plan) {
+  const vpce::TileShape ts = vpce::tile_shape(prob->dtype);
+  std::vector<Chunk> chunks;
+  bool first = true;
+  for (int i = 0; i < prob->P; ++i) {
+    const int q = prob->order ? prob->order[i] : i;
+    const int64_t Vq = prob->shard_rows[q];
+    if (Vq == 0) continue;
+    const int64_t vc =
+        std::min<int64_t>(plan.Vc, round_up(ceil_div(Vq, ceil_div(Vq, plan.Vc)), ts.grad_bm));
+    for (int64_t v0 = 0; v0 < Vq; v0 += vc) {
+      for (int64_t t0 = 0; t0 < prob->T; t0 += plan.Tc)
+        chunks.push_back({q, v0, std::min<int64_t>(vc, Vq - v0), t0,
+                          std::min<int64_t>(plan.Tc, prob->T - t0), t0 == 0, first});
+      first = false;
+    }
+  }
+  return chunks;
+}
+
 }  // namespace
 
 extern "C" {
@@ -319,35 +348,6 @@ vp_status vp_ce_fold_finalize(const vp_problem* prob, const int64_t* targets, co
   return vpce::run_fold_finalize(f, s) ? VP_OK : VP_ERR_HIP;
 }
 
-// The strips of a backward call in visiting order: shards in `order`, each cut
-// into balanced, tile-aligned vocabulary chunks (never above Vc), each chunk
-// meeting every token chunk.
-struct Chunk {
-  int q;
-  int64_t v0, M, t0, N;
-  bool new_vchunk, first_vchunk;
-};
-
-std::vector<Chunk> strip_chunks(const vp_problem* prob, const StripPlan& plan) {
-  const vpce::TileShape ts = vpce::tile_shape(prob->dtype);
-  std::vector<Chunk> chunks;
-  bool first = true;
-  for (int i = 0; i < prob->P; ++i) {
-    const int q = prob->order ? prob->order[i] : i;
-    const int64_t Vq = prob->shard_rows[q];
-    if (Vq == 0) continue;
-    const int64_t vc =
-        std::min<int64_t>(plan.Vc, round_up(ceil_div(Vq, ceil_div(Vq, plan.Vc)), ts.grad_bm));
-    for (int64_t v0 = 0; v0 < Vq; v0 += vc) {
-      for (int64_t t0 = 0; t0 < prob->T; t0 += plan.Tc)
-        chunks.push_back({q, v0, std::min<int64_t>(vc, Vq - v0), t0,
-                          std::min<int64_t>(plan.Tc, prob->T - t0), t0 == 0, first});
-      first = false;
-    }
-  }
-  return chunks;
-}
-
 vp_status vp_ce_plan_info(const vp_problem* prob, vp_plan_info* info) {
   const vp_status st = validate(prob, nullptr);
   if (st != VP_OK) return st;
@@ -412,11 +412,9 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
     tr.in = H;
     tr.ld_in = d;
     tr.out = Ht;
-    tr.ld_out = plan.T_pad;
     tr.R = (int32_t)T;
     tr.C = (int32_t)d;
     tr.R_pad = (int32_t)plan.T_pad;
-    tr.blocked = 1;
     if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
   }
 
@@ -468,11 +466,9 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
         tr.in = wchunk(c);
         tr.ld_in = d;
         tr.out = Wt;
-        tr.ld_out = plan.Vc;
         tr.R = (int32_t)c.M;
         tr.C = (int32_t)d;
         tr.R_pad = (int32_t)round_up(c.M, KB);  // >= the K the dH launch reads
-        tr.blocked = 1;
         if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
       }
       // dH[t0 : t0+N] (+)= G^T W_chunk = G^T . (W^T)^T

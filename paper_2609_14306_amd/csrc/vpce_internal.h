@@ -102,17 +102,16 @@ struct GemmArgs {
   int64_t kblka, kblkb;
 };
 
-// out[c][r] = in[r][c] for r < R (zero for R <= r < R_pad), c < C.  blocked == 0:
-// out is row-major with pitch ld_out; blocked != 0: out is k-blocked in 128-byte
-// blocks of KB elements (64 bfloat16, 32 float32), [R_pad/KB][C][KB] (element
-// (c, r) at ((r / KB) C + c) KB + r % KB).
+// out[c][r] = in[r][c] for r < R (zero for R <= r < R_pad), c < C.  in is
+// row-major with pitch ld_in; out is k-blocked in 128-byte blocks of KB elements
+// (64 bfloat16, 32 float32), [R_pad/KB][C][KB] (element (c, r) at
+// ((r / KB) C + c) KB + r % KB).  C and ld_in are whole 16-byte vectors, R_pad a
+// multiple of KB.
 struct TransposeArgs {
   const void* in;
   int64_t ld_in;
   void* out;
-  int64_t ld_out;
   int32_t R, C, R_pad;
-  int32_t blocked;
 };
 
 struct TileShape {

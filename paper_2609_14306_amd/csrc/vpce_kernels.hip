@@ -957,30 +957,49 @@ __global__ void __launch_bounds__(GM::NT, GM::OCC)
   grad_tile<E, GL>(g, mt, nt, smem);
 }
 
-// out[c][r] = in[r][c] through a 64 x 64 LDS tile; rows R..R_pad-1 of the
-// output's columns are zero-filled.  One-dimensional grid of row-block-fastest
-// 64 x 64 tiles (either side alone can exceed 65535 blocks: T / 64 up to 2^17,
-// d / 64 up to 2^16).
+// out = in^T in the k-blocked layout: in is row-major [R][ld_in]; out is
+// [R_pad / KB][C][KB] with KB = 128 / sizeof(S) (element (c, r) at
+// ((r / KB) C + c) KB + r % KB), zero for R <= r < R_pad.  One 64 x 64 tile per
+// workgroup (one-dimensional grid, row blocks fastest: T / 64 up to 2^17 and
+// d / 64 up to 2^16 exceed a grid dimension), staged through LDS with 16-byte
+// accesses to global memory on both sides.  A tile row of 64 elements is VPR
+// 16-byte vectors; vector v of tile row i sits in slot v ^ ((i / VEC) % VPR), so
+// that the column reads of the store side (VEC consecutive rows of one column
+// per lane, rows VEC g .. VEC g + VEC - 1 for lane group g) fall in distinct
+// banks.  Needs C, ld_in and both base addresses in whole 16-byte vectors and
+// R_pad a multiple of KB (checked by run_transpose).
 template <class S>
 __global__ void __launch_bounds__(256) transpose_kernel(TransposeArgs a) {
-  __shared__ S tile[64][65];
+  constexpr int VEC = 16 / (int)sizeof(S);  // elements per 16-byte vector
+  constexpr int VPR = 64 / VEC;             // vectors per tile row
+  constexpr int ROWS = 256 / VPR;           // tile rows (or output rows) per pass
+  constexpr int KB = 128 / (int)sizeof(S);
+  __shared__ __attribute__((aligned(16))) S tile[64][64];
   const S* in = (const S*)a.in;
   S* out = (S*)a.out;
   const uint32_t n_rb = ((uint32_t)a.R_pad + 63u) / 64u;
   const int r0 = (int)(blockIdx.x % n_rb) * 64, c0 = (int)(blockIdx.x / n_rb) * 64;
-  const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
-  for (int i = ty; i < 64; i += 4) {
-    const int r = r0 + i, c = c0 + tx;
-    tile[i][tx] = (r < a.R && c < a.C) ? in[(int64_t)r * a.ld_in + c] : (S)0;
+  const int v = threadIdx.x % VPR, i0 = threadIdx.x / VPR;
+#pragma unroll
+  for (int i = i0; i < 64; i += ROWS) {
+    const int r = r0 + i, c = c0 + VEC * v;
+    uint4 x = make_uint4(0u, 0u, 0u, 0u);
+    if (r < a.R && c < a.C) x = *(const uint4*)(in + (int64_t)r * a.ld_in + c);
+    *(uint4*)&tile[i][(v ^ ((i / VEC) % VPR)) * VEC] = x;
   }
   __syncthreads();
-  for (int i = ty; i < 64; i += 4) {
-    const int c = c0 + i, r = r0 + tx;
+  // lane group g = v gathers tile rows VEC g .. VEC g + VEC - 1 of one column
+#pragma unroll
+  for (int cl = i0; cl < 64; cl += ROWS) {
+    const int c = c0 + cl, r = r0 + VEC * v;
     if (c < a.C && r < a.R_pad) {
-      constexpr int KB = 128 / (int)sizeof(S);  // elements of a 128-byte k-block
-      const int64_t o = a.blocked ? ((int64_t)(r / KB) * a.C + c) * KB + (r % KB)
-                                  : (int64_t)c * a.ld_out + r;
-      out[o] = tile[tx][i];
+      union {
+        uint4 u;
+        S e[VEC];
+      } y;
+#pragma unroll
+      for (int j = 0; j < VEC; ++j) y.e[j] = tile[VEC * v + j][((cl / VEC) ^ v) * VEC + cl % VEC];
+      *(uint4*)(out + ((int64_t)(r / KB) * a.C + c) * KB + r % KB) = y.u;
     }
   }
 }
@@ -1164,6 +1183,11 @@ bool run_bwd_stage(int dtype, const GemmArgs& h, const GemmArgs& w, const GradAr
 }
 bool run_transpose(int dtype, const TransposeArgs& a, hipStream_t s) {
   if (a.C <= 0 || a.R_pad <= 0) return true;
+  const int esz = dtype == 1 ? 2 : 4, vec = 16 / esz, kb = 128 / esz;
+  // the 16-byte accesses of the kernel: whole vectors on both sides, whole k-blocks
+  if (a.C % vec != 0 || a.ld_in % vec != 0 || a.R_pad % kb != 0 || a.R < 0 || a.R > a.R_pad ||
+      ((uintptr_t)a.in & 15u) != 0 || ((uintptr_t)a.out & 15u) != 0)
+    return false;
   const int64_t blocks = (int64_t)((a.R_pad + 63) / 64) * ((a.C + 63) / 64);
   if (blocks > 0x7fffffff) return false;  // beyond any operand that fits in memory
   const dim3 grid((unsigned)blocks);
