@@ -346,7 +346,19 @@ def main():
                          "counters": measured_clock("fwd_kernel", w.name)},
         "bad_targets": bad,
         "input_gen_s": t_gen,
+        # The paper's own figures for this path (context, not a target: other hardware, FP32,
+        # eight GPUs): peak allocation of the projection forward + backward per rank, standard
+        # dense projection against Ring-DTP (Sec. 3.2 results table, App. C peak table).
+        "paper_context": {"hardware": "one node of 8x NVIDIA H200, FP32",
+                          "shape": "N=16384 tokens per rank, H=7168, V=200000, P=8",
+                          "projection_peak_gib": {"standard": 42.462, "ring_dtp": 7.322},
+                          "increment_over_resident_gib": {"standard": 36.6212, "ring_dtp": 6.1545},
+                          "latency_ms": {"standard": 1001.2, "ring_dtp": 1052.2}},
     }
+    for key in ("roofline", "roofline_fwd"):  # HBM rate of the counted traffic
+        r = out[key]
+        r["traffic_gb_per_s"] = (r["traffic"] / (r["avg_launch_ms"] * 1e-3) / 1e9
+                                 if r["traffic"] is not None else None)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(inp, args.cpu_sample_rows)
     print(json.dumps(out), flush=True)
