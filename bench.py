@@ -210,7 +210,7 @@ def cpu_baseline(inp, rows: int):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on exactly one GPU (one device's share of "
+        print(json.dumps({"error": "the benchmark runs on exactly one GPU (one device's share of "
                                    "the ring); --gpus must be 1", "n_gpus": args.gpus}))
         sys.exit(2)
 

@@ -60,7 +60,7 @@ typedef enum {
   VP_ERR_WORKSPACE = 6,   /* workspace pointer NULL or smaller than the size the library asked for */
   VP_ERR_TARGET = 7,      /* (vp_ce_check) some target was outside [0, V) and not ignore_index */
   VP_ERR_HIP = 8,         /* a HIP runtime call or a kernel launch failed */
-  VP_ERR_UNSUPPORTED = 9  /* valid request this build does not implement */
+  VP_ERR_UNSUPPORTED = 9  /* valid request the library does not implement */
 } vp_status;
 
 typedef enum {
