@@ -6,7 +6,11 @@ bench.py times (default strip budget, the workload's visiting order).
 * dH on a seeded sample of token rows and dW on a seeded sample of vocabulary
   ids (every shard's first and last id, the most frequent targets, random ids),
   each computed by the oracle at test time from the full-size inputs;
-* the exact properties: ignored tokens have loss 0 and zero dH rows.
+* the exact properties: ignored tokens have loss 0 and zero dH rows;
+* every token's residual row sums to zero over the vocabulary, so the sum of all
+  rows of dW is zero: checked on every dW row at once, against the same 1e-2 of
+  the dW Frobenius norm (independent row errors of relative size e add up to
+  about e times that norm).
 
 Tolerances as everywhere for bf16: |d loss|, |d lse| <= 2e-3; relative Frobenius
 error <= 1e-2 on the sampled dH rows and on the sampled dW rows.
@@ -75,3 +79,13 @@ def test_fullsize_sampled_parity(name):
                        for v in ids])
     e2 = assert_grad_close("bf16", got_dW, ref_dW, f"{name} dW rows")
     print(f"{name}: dH rows rel-Fro {e:.2e}, dW rows rel-Fro {e2:.2e}", flush=True)
+
+    col_sum = torch.zeros(d, dtype=torch.float64, device=dWs[0].device)
+    fro2 = 0.0
+    for w in dWs:
+        w64 = w.double()
+        col_sum += w64.sum(0)
+        fro2 += float((w64 * w64).sum())
+    rel_sum = float(col_sum.norm()) / max(fro2 ** 0.5, 1e-300)
+    print(f"{name}: |sum_v dW_v| / |dW|_F = {rel_sum:.2e}", flush=True)
+    assert rel_sum <= 1e-2, f"{name}: dW rows do not sum to zero ({rel_sum:.2e})"
