@@ -575,29 +575,46 @@ __global__ void __launch_bounds__(G::NT, G::OCC) fwd_kernel(FwdArgs a) {
       for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
     G::run(acc, Wt, a.d, 0, rows, (const S*)a.H, a.d, n0, (int)a.T, a.d, smem);
 
+    // Tiles past the end of a shard mask their padded rows; full tiles (all but the
+    // last of each shard) take the select-free loops.
     const bool full = rows == BM;
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
+      // The maximum is taken on the raw logits and scaled once: scaling by a positive
+      // constant is monotone under rounding, so this equals the maximum of the scaled
+      // values.
       float tmax = -INFINITY;
+      if (full) {
 #pragma unroll
-      for (int i = 0; i < MB; ++i)
+        for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const float y2 = acc[i][j][r] * kLog2e;
-          const bool ok = full || (wm + 32 * i + acc_row(r, lane) < rows);
-          tmax = ok ? fmaxf(tmax, y2) : tmax;
-        }
+          for (int r = 0; r < 16; ++r) tmax = fmaxf(tmax, acc[i][j][r]);
+      } else {
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r)
+            if (wm + 32 * i + acc_row(r, lane) < rows) tmax = fmaxf(tmax, acc[i][j][r]);
+      }
+      tmax *= kLog2e;
       const float scale = tmax > m_run[j] ? __builtin_amdgcn_exp2f(m_run[j] - tmax) : 1.f;
       m_run[j] = fmaxf(m_run[j], tmax);
       float sum = 0.f;
+      if (full) {
 #pragma unroll
-      for (int i = 0; i < MB; ++i)
+        for (int i = 0; i < MB; ++i)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const bool ok = full || (wm + 32 * i + acc_row(r, lane) < rows);
-          const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r], kLog2e, -m_run[j]));
-          sum += ok ? e : 0.f;
-        }
+          for (int r = 0; r < 16; ++r)
+            sum += __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r], kLog2e, -m_run[j]));
+      } else {
+#pragma unroll
+        for (int i = 0; i < MB; ++i)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r], kLog2e, -m_run[j]));
+            sum += (wm + 32 * i + acc_row(r, lane) < rows) ? e : 0.f;
+          }
+      }
       s_run[j] = s_run[j] * scale + sum;
 
       // Target gather: exactly one tile in the whole vocabulary holds the target.
