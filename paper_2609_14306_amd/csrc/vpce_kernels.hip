@@ -49,10 +49,13 @@ struct Bf16 {
   __device__ static f32x16_t mma16(frag16 a, frag16 b, f32x16_t c) {
     return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
   }
-  __device__ static storage from_f32(float x) {  // round to nearest even (NaN stays NaN)
-    uint32_t u = __float_as_uint(x);
-    u += 0x7FFFu + ((u >> 16) & 1u);
-    return (storage)(u >> 16);
+  // Two float32 values rounded to nearest even, packed low then high (one
+  // v_cvt_pk_bf16_f32).
+  __device__ static uint32_t pack2(float lo, float hi) {
+    typedef float f32x2_t __attribute__((ext_vector_type(2)));
+    typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+    const f32x2_t v = {lo, hi};
+    return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2_t));
   }
 };
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
@@ -73,7 +76,6 @@ struct F32 {
     c = __builtin_amdgcn_mfma_f32_32x32x2f32(a[2], b[2], c, 0, 0, 0);
     return __builtin_amdgcn_mfma_f32_32x32x2f32(a[3], b[3], c, 0, 0, 0);
   }
-  __device__ static storage from_f32(float x) { return x; }
 };
 
 // ---------------------------------------------------------------------------
@@ -827,19 +829,18 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
       for (int r4 = 0; r4 < 16; r4 += 4) {
         // registers r4..r4+3 hold 4 consecutive vocabulary rows of token column nl
         const int ml0 = m0 + wm + 32 * i + acc_row(r4, lane);
-        S v4[4];
+        float v4[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
           const int ml = ml0 + q;
           const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r4 + q], kLog2e, -lse2));
-          const float v = (live && ml < a.M) ? g * (p - (rel == ml ? 1.f : 0.f)) : 0.f;
-          v4[q] = E::from_f32(v);
+          v4[q] = (live && ml < a.M) ? g * (p - (rel == ml ? 1.f : 0.f)) : 0.f;
           if constexpr (!kBlocked)
             Gs[(((uint32_t)nl / KB) * Vc + (uint32_t)ml) * KB + (uint32_t)nl % KB] = v4[q];
         }
         if constexpr (kBlocked) {
-          packed[j][i][r4 >> 2].x = (uint32_t)v4[0] | ((uint32_t)v4[1] << 16);
-          packed[j][i][r4 >> 2].y = (uint32_t)v4[2] | ((uint32_t)v4[3] << 16);
+          packed[j][i][r4 >> 2].x = E::pack2(v4[0], v4[1]);
+          packed[j][i][r4 >> 2].y = E::pack2(v4[2], v4[3]);
         } else {  // 4 consecutive vocabulary rows: one 16-byte store into a 32-wide k-block
           *(float4*)(Gt + (((uint32_t)ml0 / KB) * Tc + (uint32_t)nl) * KB + (uint32_t)ml0 % KB) =
               make_float4(v4[0], v4[1], v4[2], v4[3]);
