@@ -16,7 +16,8 @@ namespace {
 
 constexpr size_t kHeaderBytes = 256;       // error counter + reserved
 constexpr int64_t kDefaultStrip = 100ll << 20;  // residual-strip budget in elements per layout
-constexpr int kTargetGroups = 512;         // forward workgroups to aim for (2 per CU on 256 CUs)
+constexpr int64_t kCUs = 256;                      // compute units of one MI355X
+constexpr int64_t kPanelCacheBudget = 160ll << 20;  // of the 256 MiB memory-side cache
 constexpr int kMaxSplits = 32;
 
 inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
@@ -60,10 +61,25 @@ vp_status validate(const vp_problem* p, int64_t* V_out, bool allow_empty_vocab =
 
 inline bool misaligned(const void* ptr) { return ((uintptr_t)ptr & 15u) != 0; }
 
+// Vocabulary splits of the forward: workgroup (token block, split) folds one token
+// block over one contiguous range of the vocabulary tiles, and an XCD runs 32
+// consecutive workgroups at a time, i.e. 32 / S token blocks by S splits.  S is the
+// smallest power of two (at most 32) that
+// - fills the CUs (token blocks x S >= 256);
+// - is at least 4, so that those 32 tiles share 12 operand panels in the XCD's L2
+//   (8 x 4 or 4 x 8);
+// - keeps the H panels of the 256 / S token blocks running at once within 160 MiB,
+//   so that they stay in the memory-side cache while every vocabulary tile re-reads
+//   them.
 int splits_for(const vp_problem* p) {
   const vpce::TileShape ts = vpce::tile_shape(p->dtype);
   const int64_t tok_blocks = std::max<int64_t>(1, ceil_div(p->T, ts.fwd_bn));
-  return (int)std::min<int64_t>(kMaxSplits, std::max<int64_t>(1, ceil_div(kTargetGroups, tok_blocks)));
+  const int64_t panel = (int64_t)ts.fwd_bn * p->d * (int64_t)elem_bytes(p->dtype);
+  const int64_t need = std::max<int64_t>(
+      4, std::max(ceil_div(kCUs, tok_blocks), ceil_div(kCUs * panel, kPanelCacheBudget)));
+  int s = 4;
+  while (s < need && s < kMaxSplits) s *= 2;
+  return s;
 }
 
 size_t fwd_ws_bytes(const vp_problem* p) {
