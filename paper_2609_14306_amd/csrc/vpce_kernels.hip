@@ -1036,10 +1036,9 @@ template <> struct Cfg<Bf16> {
   // 17% slower: a lone wave's load-issue stalls and barrier waits idle the MFMA
   // pipe.
   using Logits = GemmDma<256, 256, 2, 4>;
-  using MmA = GemmDma<256, 256, 2, 4>;
-  using MmB = MmA;
+  using Mm = Logits;  // the dH / dW contractions
   using LogitsReg = Gemm<Bf16, Logits::BM, Logits::BN, Logits::WGM, Logits::WGN>;
-  static_assert(64 % MmA::KDIV == 0 && 64 % MmB::KDIV == 0, "dH / dW launch granularity");
+  static_assert(64 % Mm::KDIV == 0, "dH / dW launch granularity");
   static constexpr int KALIGN = 64;  // K granularity the dH / dW launches need
 };
 template <> struct Cfg<F32> {
@@ -1047,8 +1046,7 @@ template <> struct Cfg<F32> {
   // four 32x32x2 f32 MFMAs per fragment pair.  d not a multiple of 32: the
   // register-staged tile of the same shape.
   using Logits = GemmDma<256, 256, 2, 4, 64, 2, F32>;
-  using MmA = Logits;
-  using MmB = MmA;
+  using Mm = Logits;  // the dH / dW contractions
   using LogitsReg = Gemm<F32, Logits::BM, Logits::BN, Logits::WGM, Logits::WGN>;
   static constexpr int KALIGN = 32;  // K granularity the dH / dW launches need
 };
@@ -1116,18 +1114,11 @@ static bool launch_stage_g(const GemmArgs& h, const GemmArgs& w, const GradArgs&
                      g, sp);
   return launched_ok();
 }
-template <class E, class GL>
-static bool launch_stage_l(const GemmArgs& h, const GemmArgs& w, const GradArgs& g, hipStream_t s) {
-  // dH and dW share N (= d)
-  const int N = h.M > 0 ? h.N : w.N;
-  if (N % 256 != 0 && N % 192 == 0)
-    return launch_stage_g<E, GL, typename Cfg<E>::MmB>(h, w, g, s);
-  return launch_stage_g<E, GL, typename Cfg<E>::MmA>(h, w, g, s);
-}
 template <class E>
 static bool launch_stage(const GemmArgs& h, const GemmArgs& w, const GradArgs& g, hipStream_t s) {
-  if (g.d % Cfg<E>::Logits::KDIV == 0) return launch_stage_l<E, typename Cfg<E>::Logits>(h, w, g, s);
-  return launch_stage_l<E, typename Cfg<E>::LogitsReg>(h, w, g, s);
+  using Mm = typename Cfg<E>::Mm;
+  if (g.d % Cfg<E>::Logits::KDIV == 0) return launch_stage_g<E, typename Cfg<E>::Logits, Mm>(h, w, g, s);
+  return launch_stage_g<E, typename Cfg<E>::LogitsReg, Mm>(h, w, g, s);
 }
 
 // ---- entry points used by the host API (vpce_api.cpp) ----
