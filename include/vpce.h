@@ -90,8 +90,9 @@ typedef struct {
 /* Workspace sizes in bytes for vp_ce_forward (*fwd_bytes) and vp_ce_backward
  * (*bwd_bytes); either output pointer may be NULL.  Host only, needs no device.
  * forward: per-token partial states of the vocabulary splits, O(T);
- * backward: the residual strip in two layouts (2 x strip_elems elements at
- * most), H^T (T x d elements) and W^T of one vocabulary chunk (d x strip
+ * backward: the residual strip in two layouts, twice (one being written while
+ * the other is contracted: 4 x strip_elems elements at most), H^T (T x d
+ * elements, T rounded up to 256) and W^T of one vocabulary chunk (d x strip
  * columns).  Neither depends on V. */
 vp_status vp_ce_workspace_size(const vp_problem* prob, size_t* fwd_bytes, size_t* bwd_bytes);
 
