@@ -330,7 +330,7 @@ def main():
         # dH and dW tiles), launched once per strip plus once.  Its average launch
         # carries 6TVd / launches flops; its average duration is taken as the backward
         # call's event time over the launch count (the call also holds the H and W
-        # transposes, about 1% of it, so achieved is slightly understated).
+        # transposes, about 0.5% of it, so achieved is slightly understated).
         "roofline": {"kernel": "bwd_stage_kernel (logits recompute + residual + dH + dW MFMA tiles)",
                      "bound": "mfma", "achieved": bwd_tflops, "peak": peak, "unit": "TFLOP/s",
                      "frac": bwd_tflops / peak, "traffic": bwd_traffic,
