@@ -61,6 +61,29 @@ def test_workspace_size_independent_of_V():
     assert 0 < bwd <= 4 * (100 << 20) * eb + T * d * eb + d * 32768 * eb + 8192
 
 
+def _forward_splits(T, d, dtype, shard_rows=(25136,) * 8):
+    """The forward's vocabulary split count S, read back from its workspace size:
+    256 header bytes, S partial maxima and sums per token, one target logit per token."""
+    fwd, _ = vp.vp_ce_workspace_size(_prob(T=T, d=d, dtype=dtype, shard_rows=list(shard_rows)))
+    a256 = lambda x: (x + 255) // 256 * 256
+    body = fwd - 256 - a256(T * 4)
+    S = body // 2 // (T * 4)
+    assert 2 * a256(S * T * 4) == body
+    return S
+
+
+@pytest.mark.parametrize("T, d, dtype, S", [
+    (256, 256, vp.VP_F32, 32),        # one token block: splits fill the CUs, at most 32
+    (4096, 2880, vp.VP_BF16, 16),     # 16 token blocks: 16 splits fill 256 CUs
+    (32768, 2880, vp.VP_BF16, 4),     # at least 4: 32 concurrent tiles share 12 panels
+    (16384, 7168, vp.VP_BF16, 8),     # 64 H panels of 3.7 MB would overflow the cache budget
+    (65536, 4096, vp.VP_BF16, 4),     # 64 H panels of 2 MB fit; 2 splits would not
+    (16384, 7168, vp.VP_F32, 16),     # float32 panels are twice the bytes
+])
+def test_forward_split_rule(T, d, dtype, S):
+    assert _forward_splits(T, d, dtype) == S
+
+
 def test_largest_accepted_shapes():
     fwd, bwd = vp.vp_ce_workspace_size(_prob(T=(1 << 23) - 256))
     assert fwd > 0 and bwd > 0
