@@ -10,10 +10,10 @@
 // The backward stores the softmax residual of a (vocabulary chunk, token
 // chunk) strip in both layouts (G and G^T) and uses transposed copies of H
 // (once per call) and of each vocabulary chunk of W, so that every operand is
-// staged k-contiguous and every MFMA fragment is one 16-byte LDS read (on
-// gfx950 the LDS transpose read sustains well under half the bandwidth of a
-// plain 16-byte read, and transposing in registers costs VALU work and LDS
-// bank conflicts).
+// staged k-contiguous and every MFMA fragment is one 16-byte LDS read (an
+// operand read through gfx950's LDS transpose read, two 8-byte reads per
+// fragment, costs the mainloop about 4% of its rate, more than the second
+// layout and the transposes cost).
 //
 // Logits are computed transposed (vocabulary rows, token columns) so that in the
 // MFMA accumulator layout every lane owns whole token columns: the online
@@ -1023,9 +1023,10 @@ __global__ void __launch_bounds__(256) transpose_kernel(TransposeArgs a) {
 }
 
 // ---------------------------------------------------------------------------
-// Tile configurations.  bf16: the direct-to-LDS ring (BK = 64, two slots); the
-// register-staged tile when d is not a multiple of 64.  f32: 64 x 64 tiles,
-// 256 threads (waves 2 x 2), register-staged.
+// Tile configurations.  Both element types: the direct-to-LDS ring (128-byte
+// slice rows: 64 bfloat16 or 32 float32 k values, two slots) with 256 x 256
+// tiles; the register-staged tile of the same shape when d is not a multiple of
+// the slice depth.
 template <class E> struct Cfg;
 template <> struct Cfg<Bf16> {
   // 512-thread workgroups (two wavefronts per SIMD), 256 x 256 tiles, 128 x 64 per
