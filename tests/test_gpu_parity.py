@@ -25,10 +25,13 @@ def test_tiny_f32_full_workload():
     assert got["bad_fwd"] == 0 and got["bad_bwd"] == 0
 
 
+@pytest.mark.parametrize("d", [200, 448, 576])
 @pytest.mark.parametrize("dtype_name", ["tiny_f32_T256_d256_V2048_P8", "bf16_T4096_d2880_V201088_P8"])
-def test_ragged_shards_and_tiles(dtype_name):
+def test_ragged_shards_and_tiles(dtype_name, d):
     # T, d and every shard length off the tile grid; an empty shard; a permuted order.
-    inp = _case(dtype_name, T=333, d=200, V=1100, P=1, seed=3)
+    # The last 256-wide column block of the dH / dW tiles holds 200, 192 and 64 live
+    # rows of d, so its tiles issue 4, 3 and 1 of the 4 A load groups of a slice.
+    inp = _case(dtype_name, T=333, d=d, V=1100, P=1, seed=3)
     inp = wl.resplit(inp, [100, 0, 257, 131, 612], order=[3, 0, 4, 1, 2])
     g = wl.random_grad_loss(inp.T, 3, "random")
     got = run_gpu(inp, g)
