@@ -58,3 +58,16 @@ def test_committed_profiles_name_the_default_workload():
         text = open(path).read()
         assert f"- workload: `{bench.DEFAULT_WORKLOAD}`" in text
         assert "- kernel_source_sha256: `" in text
+
+
+def test_more_than_one_gpu_is_refused():
+    # one GPU's share of the ring: the benchmark refuses other GPU counts before any GPU work
+    import json
+    import subprocess
+    import sys
+
+    r = subprocess.run([sys.executable, bench.__file__, "--gpus", "2"], capture_output=True, text=True,
+                       timeout=120)
+    assert r.returncode == 2
+    line = json.loads(r.stdout.strip().splitlines()[-1])
+    assert "exactly one GPU" in line["error"] and line["n_gpus"] == 2
