@@ -8,7 +8,7 @@ It holds none of the method's arithmetic and is the only code that both the
 CPU oracle side (tests) and the HIP side (tests, bench) share.
 
 Recipe (shapes and distributions of the paper's isolated vocabulary-projection
-benchmark, Sec. 3.2 and its appendix table of the projection; sizes of the five
+benchmark, Sec. 3.2 and its appendix table of the projection; sizes of the
 named workloads below):
 
 * one ``numpy.random.default_rng(seed)`` stream (PCG64), drawn in this order:
