@@ -68,8 +68,9 @@ def _residual_chunk(Y: np.ndarray, lse: np.ndarray, t: np.ndarray, g: np.ndarray
 
 
 def forward(H: np.ndarray, W: np.ndarray, targets: np.ndarray, ignore_index: int = -100,
-            row_chunk: Optional[int] = None) -> Tuple[np.ndarray, np.ndarray]:
-    """Per-token (loss, lse) in float64 from the full logits of each row chunk."""
+            row_chunk: Optional[int] = None, return_max_abs: bool = False):
+    """Per-token (loss, lse) in float64 from the full logits of each row chunk; with
+    return_max_abs, also the largest |y_tv| over every token and vocabulary id."""
     H = np.asarray(H, dtype=np.float64)
     W = np.asarray(W, dtype=np.float64)
     targets = np.asarray(targets, dtype=np.int64)
@@ -77,10 +78,15 @@ def forward(H: np.ndarray, W: np.ndarray, targets: np.ndarray, ignore_index: int
     rc = row_chunk or _default_chunk(W.shape[0])
     loss = np.zeros(T)
     lse = np.zeros(T)
+    max_abs = 0.0
     for a in range(0, T, rc):
         b = min(T, a + rc)
         Y = H[a:b] @ W.T
+        if Y.size:
+            max_abs = max(max_abs, float(np.max(np.abs(Y))))
         loss[a:b], lse[a:b] = _forward_chunk(Y, targets[a:b], ignore_index)
+    if return_max_abs:
+        return loss, lse, max_abs
     return loss, lse
 
 

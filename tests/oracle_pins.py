@@ -324,6 +324,71 @@ def pin_out_of_range_target(ce):
     assert np.all(np.isnan(dH[2])) and np.all(np.isfinite(np.delete(dH, 2, axis=0)))
 
 
+def pin_max_abs_logit(ce):
+    """The largest |logit| both dense functions report equals a pure-Python scan of every
+    h_t . w_v (the stress workload's logit scale is read from it)."""
+    H, W, t, g, shards = _problem(13, T=7, d=4, V=9, rows=(4, 5), ignore=(2,), scale=2.0)
+    # the largest magnitude sits in an interior token row, which is in neither the first
+    # nor the last row chunk when the rows are cut into chunks of 1 to 3
+    H[3] *= 6.0
+    want = 0.0
+    for i in range(H.shape[0]):
+        for v in range(W.shape[0]):
+            want = max(want, abs(sum(float(H[i, k]) * float(W[v, k]) for k in range(H.shape[1]))))
+    _, _, got = ce.forward(H, W, t, IGN, return_max_abs=True)
+    assert abs(got - want) <= 1e-13 * want, (got, want)
+    got_fb = ce.forward_backward(H, shards, t, g, IGN)["max_abs_logit"]
+    assert abs(got_fb - want) <= 1e-13 * want, (got_fb, want)
+
+
+class _RowChunked:
+    """The oracle with every row-chunked entry point forced to a given row chunk.
+
+    The dense functions split the token rows into independent chunks (only dW sums
+    across them).  The pins above use shapes far below the default chunk, so they run
+    one chunk; through this view they run with chunks of 1, 2 and 3 rows, i.e. with
+    every token in a chunk of its own, with chunk edges inside the batch and with a
+    short last chunk.  Attributes are looked up on the wrapped module at call time, so
+    a planted mistake in it is seen through the view."""
+
+    _CHUNKED = ("forward", "backward", "forward_backward", "forward_rows", "backward_rows",
+                "dW_rows")
+
+    def __init__(self, ce, rc):
+        self._ce = ce
+        self._rc = rc
+
+    def __getattr__(self, name):
+        fn = getattr(self._ce, name)
+        if name not in self._CHUNKED:
+            return fn
+        rc = self._rc
+
+        def chunked(*args, **kw):
+            kw["row_chunk"] = rc
+            return fn(*args, **kw)
+        return chunked
+
+
+_CHUNK_PINS = (pin_golden_closed_form, pin_torch_cross_entropy, pin_finite_differences,
+               pin_ignore_masking, pin_two_class_logistic, pin_restrictions,
+               pin_zero_hidden_closed_form, pin_invariants, pin_scalar_loops, pin_max_abs_logit)
+
+
+def pin_row_chunk_loop(ce):
+    """The closed forms, library routine, finite differences, masking, two-class and
+    restriction pins again with the token rows cut into chunks of 1, 2 and 3 rows, through
+    every entry point that takes a row chunk (the full-size expected values are written by
+    the same loop over many chunks)."""
+    for rc in (1, 2, 3):
+        view = _RowChunked(ce, rc)
+        for pin in _CHUNK_PINS:
+            try:
+                pin(view)
+            except AssertionError as e:
+                raise AssertionError(f"{pin.__name__} with row_chunk={rc}: {e}") from e
+
+
 ALL_PINS = [
     pin_golden_closed_form,
     pin_uniform_logits,
@@ -339,4 +404,6 @@ ALL_PINS = [
     pin_torch_cross_entropy,
     pin_restrictions,
     pin_out_of_range_target,
+    pin_max_abs_logit,
+    pin_row_chunk_loop,
 ]

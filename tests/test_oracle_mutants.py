@@ -10,6 +10,7 @@ import oracle.ce as ce
 from oracle_pins import ALL_PINS
 
 _orig_fwd = ce._forward_chunk
+_orig_forward = ce.forward
 _orig_res = ce._residual_chunk
 
 
@@ -116,7 +117,112 @@ def _fb_from(backward):
     return forward_backward
 
 
+# Mistakes in the row-chunk loop of the dense functions: they change nothing while the
+# whole batch fits one chunk, and every full-size expected value is written by this loop.
+def _chunk_bounds(T, rc, variant):
+    for a in range(0, T, rc):
+        b = min(T, a + rc)
+        if variant == "drop_last_row" and b < T:
+            b -= 1  # off by one at every inner chunk edge; the last chunk ends at T
+        yield a, b
+
+
+def _make_chunk_forward(variant):
+    def forward(H, W, targets, ignore_index=-100, row_chunk=None):
+        H = np.asarray(H, dtype=np.float64); W = np.asarray(W, dtype=np.float64)
+        targets = np.asarray(targets, dtype=np.int64)
+        T = H.shape[0]
+        rc = row_chunk or ce._default_chunk(W.shape[0])
+        loss, lse = np.zeros(T), np.zeros(T)
+        for a, b in _chunk_bounds(T, rc, variant):
+            loss[a:b], lse[a:b] = _orig_fwd(H[a:b] @ W.T, targets[a:b], ignore_index)
+        return loss, lse
+    return forward
+
+
+def _make_chunk_backward(variant):
+    def backward(H, W, targets, lse, grad_loss, ignore_index=-100, row_chunk=None):
+        H = np.asarray(H, dtype=np.float64); W = np.asarray(W, dtype=np.float64)
+        targets = np.asarray(targets, dtype=np.int64)
+        g = np.asarray(grad_loss, dtype=np.float64)
+        lse = np.asarray(lse, dtype=np.float64)
+        T = H.shape[0]
+        rc = row_chunk or ce._default_chunk(W.shape[0])
+        dH, dW = np.zeros_like(H), np.zeros_like(W)
+        for a, b in _chunk_bounds(T, rc, variant):
+            la = lse[0:b - a] if variant == "first_chunk_lse" else lse[a:b]
+            G = _orig_res(H[a:b] @ W.T, la, targets[a:b], g[a:b], ignore_index)
+            dH[a:b] = G @ W
+            if variant == "dW_overwritten":
+                dW = G.T @ H[a:b]
+            else:
+                dW += G.T @ H[a:b]
+        return dH, dW
+    return backward
+
+
+def _make_chunk_fb(variant):
+    def forward_backward(H, W_shards, targets, grad_loss, ignore_index=-100, row_chunk=None):
+        W = ce.concat_shards(W_shards)
+        H = np.asarray(H, dtype=np.float64)
+        targets = np.asarray(targets, dtype=np.int64)
+        g = np.asarray(grad_loss, dtype=np.float64)
+        T = H.shape[0]
+        rc = row_chunk or ce._default_chunk(W.shape[0])
+        loss, lse = np.zeros(T), np.zeros(T)
+        dH, dW = np.zeros_like(H), np.zeros_like(W)
+        for a, b in _chunk_bounds(T, rc, variant):
+            Y = H[a:b] @ W.T
+            loss[a:b], lse[a:b] = _orig_fwd(Y, targets[a:b], ignore_index)
+            la = lse[0:b - a] if variant == "first_chunk_lse" else lse[a:b]
+            G = _orig_res(Y, la, targets[a:b], g[a:b], ignore_index)
+            dH[a:b] = G @ W
+            if variant == "dW_overwritten":
+                dW = G.T @ H[a:b]
+            else:
+                dW += G.T @ H[a:b]
+        rows = [np.asarray(w).shape[0] for w in W_shards]
+        offs = np.cumsum([0] + rows)
+        return {"loss": loss, "lse": lse, "dH": dH, "dW": dW, "max_abs_logit": 0.0,
+                "dW_shards": [dW[offs[p]:offs[p + 1]] for p in range(len(rows))]}
+    return forward_backward
+
+
+def _forward_max_of_last_chunk(H, W, targets, ignore_index=-100, row_chunk=None,
+                               return_max_abs=False):
+    H = np.asarray(H, dtype=np.float64); W = np.asarray(W, dtype=np.float64)
+    targets = np.asarray(targets, dtype=np.int64)
+    T = H.shape[0]
+    rc = row_chunk or ce._default_chunk(W.shape[0])
+    loss, lse = np.zeros(T), np.zeros(T)
+    max_abs = 0.0
+    for a in range(0, T, rc):
+        b = min(T, a + rc)
+        Y = H[a:b] @ W.T
+        max_abs = float(np.max(np.abs(Y)))  # overwritten per chunk instead of a running max
+        loss[a:b], lse[a:b] = _orig_fwd(Y, targets[a:b], ignore_index)
+    return (loss, lse, max_abs) if return_max_abs else (loss, lse)
+
+
+def _forward_max_signed(H, W, targets, ignore_index=-100, row_chunk=None, return_max_abs=False):
+    out = _orig_forward(H, W, targets, ignore_index, row_chunk)
+    if not return_max_abs:
+        return out
+    Y = np.asarray(H, dtype=np.float64) @ np.asarray(W, dtype=np.float64).T
+    return out[0], out[1], float(Y.max())  # the largest logit, not the largest magnitude
+
+
+def _chunk_mutant(variant):
+    return {"forward": _make_chunk_forward(variant), "backward": _make_chunk_backward(variant),
+            "forward_backward": _make_chunk_fb(variant)}
+
+
 MUTANTS = {
+    "max_abs_logit_of_last_chunk_only": {"forward": _forward_max_of_last_chunk},
+    "max_abs_logit_signed": {"forward": _forward_max_signed},
+    "chunk_loop_dW_overwritten_per_chunk": _chunk_mutant("dW_overwritten"),
+    "chunk_loop_drops_last_row_of_chunk": _chunk_mutant("drop_last_row"),
+    "chunk_loop_lse_of_first_chunk": _chunk_mutant("first_chunk_lse"),
     "residual_without_onehot": {"_residual_chunk": _res_no_onehot},
     "residual_sign_flipped": {"_residual_chunk": _res_flipped_sign},
     "residual_without_upstream_gradient": {"_residual_chunk": _res_no_upstream},
