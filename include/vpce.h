@@ -153,9 +153,10 @@ vp_status vp_ce_state_init(float* state, int64_t T, void* stream);
  * row (id_offset + V_q <= 2^31 - 1).  H: device [T, d]; W_shard: device [V_q, d]
  * (NULL allowed when V_q == 0); targets: device int64 [T] of global ids; state as
  * above, updated in place.  ws: the forward workspace of `shard`
- * (vp_ce_workspace_size(shard, &fwd, NULL); it depends on T only, so for V_q == 0,
- * which vp_ce_workspace_size rejects, any problem with the same T gives it),
- * 16-byte aligned.  V_q == 0 or T == 0 leaves the state unchanged. */
+ * (vp_ce_workspace_size(shard, &fwd, NULL); it depends on T, d and dtype, never on
+ * V_q), 16-byte aligned.  V_q == 0 or T == 0 returns VP_OK before anything else is
+ * checked or launched and leaves the state unchanged: ws, H, W_shard, targets and
+ * state may then be NULL. */
 vp_status vp_ce_fold_shard(const vp_problem* shard, int64_t id_offset, const void* H,
                            const void* W_shard, const int64_t* targets, float* state, void* ws,
                            size_t ws_bytes, void* stream);

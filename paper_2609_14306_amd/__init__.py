@@ -144,6 +144,59 @@ def _check(status: int, what: str) -> None:
         raise VpError(status, what)
 
 
+# ---------------------------------------------------------------------------
+# Tensor checks.  The C ABI receives bare pointers: element types, widths and
+# strides are whatever the caller's tensors hold, so each tensor is checked here
+# against the problem before its pointer is taken (a wrong dtype or width would
+# make the kernels read or write outside the tensor).  Shape, dtype and layout are
+# checked first and the device last, so that every refusal is raised on the host.
+def _torch_dtype(code: int):
+    import torch
+    return torch.bfloat16 if code == VP_BF16 else torch.float32
+
+
+def _need(t, name: str, dtype, shape) -> None:
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name}: expected a torch.Tensor, got {type(t).__name__}")
+    if t.dtype != dtype:
+        raise ValueError(f"{name}: dtype {t.dtype}, expected {dtype}")
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name}: shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name}: must be contiguous (row-major)")
+
+
+def _same_device(named) -> None:
+    devs = {(t.device.type, t.device.index) for _, t in named if t is not None}
+    if len(devs) > 1:
+        raise ValueError("tensors are on different devices: " +
+                         ", ".join(f"{n} on {t.device}" for n, t in named if t is not None))
+    for n, t in named:
+        if t is not None and t.device.type != "cuda":
+            raise ValueError(f"{n}: must be on a GPU device, found {t.device}")
+
+
+def _need_ws(ws, nbytes: int):
+    import torch
+    if not isinstance(ws, torch.Tensor) or not ws.is_contiguous():
+        raise ValueError("ws: expected a contiguous torch.Tensor")
+    if ws.numel() * ws.element_size() < nbytes:
+        raise ValueError(f"ws: {ws.numel() * ws.element_size()} bytes, the call needs {nbytes}")
+
+
+def _check_inputs(prob: Problem, H, W_shards, targets):
+    import torch
+    if len(W_shards) != prob.P:
+        raise ValueError(f"W_shards: {len(W_shards)} shards, the problem has {prob.P}")
+    dt = _torch_dtype(prob.c.dtype)
+    _need(H, "H", dt, (prob.T, prob.d))
+    for p, (w, r) in enumerate(zip(W_shards, prob.shard_rows)):
+        _need(w, f"W_shards[{p}]", dt, (r, prob.d))
+    _need(targets, "targets", torch.int64, (prob.T,))
+    return [("H", H), ("targets", targets)] + [(f"W_shards[{p}]", w) for p, w in enumerate(W_shards)]
+
+
 def vp_ce_workspace_size(prob: Problem) -> Tuple[int, int]:
     f = ctypes.c_size_t(0)
     b = ctypes.c_size_t(0)
@@ -153,11 +206,21 @@ def vp_ce_workspace_size(prob: Problem) -> Tuple[int, int]:
 
 
 def vp_ce_state_init(state, T: int, stream=None) -> None:
+    import torch
+    _need(state, "state", torch.float32, (3 * int(T),))
+    _same_device([("state", state)])
     _check(load_library().vp_ce_state_init(_ptr(state), int(T), _stream(stream)), "vp_ce_state_init")
 
 
 def vp_ce_fold_shard(shard: Problem, id_offset: int, H, W_shard, targets, state, ws,
                      stream=None) -> None:
+    import torch
+    if shard.P != 1:
+        raise ValueError("vp_ce_fold_shard: the shard problem must have P == 1")
+    named = _check_inputs(shard, H, [W_shard], targets)
+    _need(state, "state", torch.float32, (3 * shard.T,))
+    _need_ws(ws, vp_ce_workspace_size(shard)[0] if shard.shard_rows[0] > 0 else 0)
+    _same_device(named + [("state", state), ("ws", ws)])
     st = load_library().vp_ce_fold_shard(ctypes.byref(shard.c), int(id_offset), _ptr(H),
                                          _ptr(W_shard) if W_shard is not None and W_shard.numel() else None,
                                          _ptr(targets), _ptr(state), _ptr(ws),
@@ -166,6 +229,13 @@ def vp_ce_fold_shard(shard: Problem, id_offset: int, H, W_shard, targets, state,
 
 
 def vp_ce_fold_finalize(prob: Problem, targets, state, loss, lse, ws, stream=None) -> None:
+    import torch
+    _need(targets, "targets", torch.int64, (prob.T,))
+    _need(state, "state", torch.float32, (3 * prob.T,))
+    _need(loss, "loss", torch.float32, (prob.T,))
+    _need(lse, "lse", torch.float32, (prob.T,))
+    _need_ws(ws, 256)
+    _same_device([("targets", targets), ("state", state), ("loss", loss), ("lse", lse), ("ws", ws)])
     st = load_library().vp_ce_fold_finalize(ctypes.byref(prob.c), _ptr(targets), _ptr(state), _ptr(loss),
                                             _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
                                             _stream(stream))
@@ -181,6 +251,12 @@ def vp_ce_plan_info(prob: Problem) -> dict:
 
 
 def vp_ce_forward(prob: Problem, H, W_shards, targets, loss, lse, ws, stream=None) -> None:
+    import torch
+    named = _check_inputs(prob, H, W_shards, targets)
+    _need(loss, "loss", torch.float32, (prob.T,))
+    _need(lse, "lse", torch.float32, (prob.T,))
+    _need_ws(ws, vp_ce_workspace_size(prob)[0])
+    _same_device(named + [("loss", loss), ("lse", lse), ("ws", ws)])
     st = load_library().vp_ce_forward(ctypes.byref(prob.c), _ptr(H), _ptr_array(W_shards), _ptr(targets),
                                       _ptr(loss), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
                                       _stream(stream))
@@ -189,6 +265,18 @@ def vp_ce_forward(prob: Problem, H, W_shards, targets, loss, lse, ws, stream=Non
 
 def vp_ce_backward(prob: Problem, H, W_shards, targets, lse, grad_loss, dH, dW_shards, ws,
                    stream=None) -> None:
+    import torch
+    named = _check_inputs(prob, H, W_shards, targets)
+    _need(lse, "lse", torch.float32, (prob.T,))
+    _need(grad_loss, "grad_loss", torch.float32, (prob.T,))
+    _need(dH, "dH", torch.float32, (prob.T, prob.d))
+    if len(dW_shards) != prob.P:
+        raise ValueError(f"dW_shards: {len(dW_shards)} shards, the problem has {prob.P}")
+    for p, (w, r) in enumerate(zip(dW_shards, prob.shard_rows)):
+        _need(w, f"dW_shards[{p}]", torch.float32, (r, prob.d))
+    _need_ws(ws, vp_ce_workspace_size(prob)[1])
+    _same_device(named + [("lse", lse), ("grad_loss", grad_loss), ("dH", dH), ("ws", ws)] +
+                 [(f"dW_shards[{p}]", w) for p, w in enumerate(dW_shards)])
     st = load_library().vp_ce_backward(ctypes.byref(prob.c), _ptr(H), _ptr_array(W_shards),
                                        _ptr(targets), _ptr(lse), _ptr(grad_loss), _ptr(dH),
                                        _ptr_array(dW_shards), _ptr(ws),

@@ -292,11 +292,12 @@ vp_status vp_ce_fold_shard(const vp_problem* shard, int64_t id_offset, const voi
   if (st != VP_OK) return st;
   if (shard->P != 1) return VP_ERR_SHAPE;
   if (id_offset < 0 || id_offset > (1ll << 31) - 1 - Vq) return VP_ERR_SHAPE;
+  const int64_t T = shard->T;
+  // an empty strip leaves the state unchanged: nothing is launched, nothing is read
+  if (T == 0 || Vq == 0) return VP_OK;
   if (!ws) return VP_ERR_WORKSPACE;
   if (ws_bytes < fwd_ws_bytes(shard)) return VP_ERR_WORKSPACE;
   if (misaligned(ws)) return VP_ERR_ALIGN;
-  const int64_t T = shard->T;
-  if (T == 0 || Vq == 0) return VP_OK;  // an empty strip leaves the state unchanged
   if (!H || !W_shard || !targets || !state) return VP_ERR_NULL;
   if (misaligned(H) || misaligned(W_shard)) return VP_ERR_ALIGN;
   if (((uintptr_t)state & 3u) != 0) return VP_ERR_ALIGN;

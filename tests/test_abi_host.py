@@ -219,9 +219,17 @@ def test_fold_argument_errors_before_launch():
     assert fold(shard, state=None) == vp.VP_ERR_NULL
     assert fold(shard, state=FAKE + 2) == vp.VP_ERR_ALIGN
     assert fold(shard, W=FAKE + 4) == vp.VP_ERR_ALIGN
-    # an empty shard or an empty batch is a no-op: nothing is launched
+    # an empty shard or an empty batch is a no-op: nothing is launched, and no workspace
+    # is needed (its size depends on T, d and dtype, which a caller may not have sized for)
     assert fold(_prob(shard_rows=[0]), W=None) == vp.VP_OK
+    assert fold(_prob(shard_rows=[0]), W=None, ws=None, ws_bytes=0) == vp.VP_OK
     assert fold(_prob(T=0, shard_rows=[1000]), H=None, t=None, state=None) == vp.VP_OK
+    assert fold(_prob(T=0, shard_rows=[1000]), H=None, t=None, state=None, ws=None,
+                ws_bytes=0) == vp.VP_OK
+    # the forward workspace depends on d and dtype as well as T (the split count does)
+    f_small, _ = vp.vp_ce_workspace_size(_prob(T=65536, d=8, shard_rows=[1000]))
+    f_wide, _ = vp.vp_ce_workspace_size(_prob(T=65536, d=7168, shard_rows=[1000]))
+    assert f_small != f_wide
     assert fold(_prob(shard_rows=[0, 0])) == vp.VP_ERR_SHAPE
 
     full = _prob(shard_rows=[1000, 24])
