@@ -51,14 +51,16 @@ def parse():
     return ap.parse_args()
 
 
-def standard_vs_fused(inp, H, Ws, tg, steps: int, warmup: int):
+def standard_vs_fused(inp, H, Ws, tg, steps: int, warmup: int, keep_outputs: bool = False):
     """The paper's comparison (its standard vs Ring-DTP table of peak memory and latency) on
     one GPU: the dense standard materialises the [T, V] logits (in the input dtype, as torch
     computes the product: bfloat16, or float32 with full float32 products), takes a float32
     log-softmax cross-entropy and backpropagates with autograd; the fused path is this
     library's forward + backward.  Both start from the same resident H, W and targets; memory
     is the peak allocation above them during a step.  The dense path is plain torch, a
-    baseline beside the product, not part of it."""
+    baseline beside the product, not part of it.  Both take the mean of the per-token losses
+    over the non-ignored tokens.  With keep_outputs, the result also holds each path's
+    per-token loss, dH and dW from its last step (key "outputs", CPU tensors)."""
     import torch
     import torch.nn.functional as F
 
@@ -93,14 +95,23 @@ def standard_vs_fused(inp, H, Ws, tg, steps: int, warmup: int):
     Hs = H.detach().clone().requires_grad_(True)
     Wsd = W.detach().clone().requires_grad_(True)
 
+    dense_last = {}
+
     def dense_step():
         Hs.grad = None
         Wsd.grad = None
         logits = Hs @ Wsd.t()
-        loss = F.cross_entropy(logits.float(), tg, ignore_index=inp.ignore_index, reduction="mean")
-        loss.backward()
+        per_tok = F.cross_entropy(logits.float(), tg, ignore_index=inp.ignore_index,
+                                  reduction="none")
+        (per_tok.sum() / max(n_valid, 1)).backward()
+        dense_last["loss"] = per_tok.detach()
 
     ms, mib = timed(dense_step, pre=lambda: (setattr(Hs, "grad", None), setattr(Wsd, "grad", None)))
+    kept = {}
+    if keep_outputs:
+        kept["standard"] = {"loss": dense_last["loss"].cpu(), "dH": Hs.grad.float().cpu(),
+                            "dW": Wsd.grad.float().cpu()}
+    dense_last.clear()
     out["standard"] = {"ms_per_step": ms, "peak_above_resident_mib": mib,
                        "what": f"logits = H W^T ({inp.dtype}, [T, V] materialised), "
                                "cross_entropy(logits.float()), autograd backward; includes the dH / dW "
@@ -113,7 +124,9 @@ def standard_vs_fused(inp, H, Ws, tg, steps: int, warmup: int):
     fwd_b, bwd_b = vp.vp_ce_workspace_size(prob)
     g = torch.full((T,), 1.0 / max(n_valid, 1), dtype=torch.float32, device=dev)
 
-    def fused_step():
+    fused_last = {}
+
+    def fused_step(keep=False):
         ws = torch.empty(max(fwd_b, bwd_b), dtype=torch.uint8, device=dev)
         loss = torch.empty(T, dtype=torch.float32, device=dev)
         lse = torch.empty(T, dtype=torch.float32, device=dev)
@@ -121,8 +134,17 @@ def standard_vs_fused(inp, H, Ws, tg, steps: int, warmup: int):
         dH = torch.empty(T, d, dtype=torch.float32, device=dev)
         dWs = [torch.empty(x.shape[0], d, dtype=torch.float32, device=dev) for x in Ws]
         vp.vp_ce_backward(prob, H, Ws, tg, lse, g, dH, dWs, ws)
+        if keep:
+            fused_last.update(loss=loss, dH=dH, dW=dWs)
 
     ms, mib = timed(fused_step)
+    if keep_outputs:  # one more step, untimed, whose outputs are kept
+        fused_step(keep=True)
+        torch.cuda.synchronize()
+        kept["fused"] = {"loss": fused_last["loss"].cpu(), "dH": fused_last["dH"].cpu(),
+                         "dW": torch.cat(fused_last["dW"], dim=0).cpu()}
+        out["outputs"] = kept
+    fused_last.clear()
     out["fused"] = {"ms_per_step": ms, "peak_above_resident_mib": mib,
                     "what": "vp_ce_forward + vp_ce_backward; workspace, loss / lse and the dH / dW "
                             "outputs allocated inside the step"}

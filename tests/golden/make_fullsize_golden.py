@@ -2,9 +2,10 @@
 
 Expected values for the full-size GPU parity tests (tests/test_gpu_fullsize.py):
 the float64 oracle's forward (Sec. 3.2: lse = log sum_v e^y, loss = lse - y_target)
-over every token of each workload, stored with the SHA-256 of the generated
-inputs so that a test can confirm it draws the same bits.  Calls only the oracle
-and the input generator.  Takes about ten minutes on eight cores.
+over every token of each workload, and the largest |logit| it met (the stress
+workload's logit scale is checked against it), stored with the SHA-256 of the
+generated inputs so that a test can confirm it draws the same bits.  Calls only
+the oracle and the input generator.  Takes about half an hour on eight cores.
 
     python tests/golden/make_fullsize_golden.py [workload ...]
 """
@@ -32,11 +33,11 @@ def make(name: str) -> None:
     sha = inp.sha256()
     H = wl.to_f64(inp.H, inp.dtype)
     W = np.concatenate([wl.to_f64(w, inp.dtype) for w in inp.W_shards], axis=0)
-    loss, lse = oracle.forward(H, W, inp.targets, inp.ignore_index)
+    loss, lse, max_abs = oracle.forward(H, W, inp.targets, inp.ignore_index, return_max_abs=True)
     np.savez_compressed(golden_path(name), loss=loss, lse=lse, sha256=np.array(sha),
-                        T=inp.T, d=inp.d, V=inp.V)
+                        T=inp.T, d=inp.d, V=inp.V, max_abs_logit=max_abs)
     print(f"{name}: T={inp.T} d={inp.d} V={inp.V} in {time.time() - t0:.0f} s, "
-          f"max lse {lse.max():.3f}", flush=True)
+          f"max lse {lse.max():.3f}, max |logit| {max_abs:.3f}", flush=True)
 
 
 if __name__ == "__main__":

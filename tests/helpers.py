@@ -120,3 +120,32 @@ def compare_all(inp: wl.Inputs, got, ref, label: str = "") -> dict:
     rw = np.concatenate([w.reshape(-1, inp.d) for w in ref["dW_shards"]], axis=0)
     e_dw = assert_grad_close(dt, gw, rw, f"{label} dW")
     return {"dH_rel_fro": e_dh, "dW_rel_fro": e_dw}
+
+
+def strip_layout(T: int, shard_rows, order, Tc: int, Vc: int, tile: int = 256):
+    """The backward's cut of the T x V residual as vp_ce_plan_info describes it: token
+    chunks of Tc, and each non-empty shard (in visiting order) cut into balanced
+    vocabulary chunks of at most Vc rows, tile-aligned.  Returns (token chunks, vocabulary
+    chunks) as lists of half-open [lo, hi) ranges; vocabulary ranges are global ids."""
+    tok = [(t0, min(T, t0 + Tc)) for t0 in range(0, T, Tc)]
+    offs = np.cumsum([0] + list(shard_rows))
+    voc = []
+    for q in order:
+        Vq = int(shard_rows[q])
+        if Vq == 0:
+            continue
+        n = -(-Vq // Vc)
+        vc = min(Vc, -(-(-(-Vq // n)) // tile) * tile)
+        for v0 in range(0, Vq, vc):
+            voc.append((int(offs[q]) + v0, int(offs[q]) + min(Vq, v0 + vc)))
+    return tok, voc
+
+
+def stratified_rows(chunks, per_chunk: int, seed: int) -> np.ndarray:
+    """Each chunk's first and last index plus `per_chunk` seeded indices inside it."""
+    rng = np.random.default_rng(seed + 15485863)
+    out = set()
+    for lo, hi in chunks:
+        out.update({lo, hi - 1})
+        out.update(rng.integers(lo, hi, size=min(per_chunk, hi - lo)).tolist())
+    return np.array(sorted(out), dtype=np.int64)

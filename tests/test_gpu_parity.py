@@ -60,6 +60,22 @@ def test_small_strip_forces_many_chunks():
     compare_all(inp, got2, ref, "default strip")
 
 
+@pytest.mark.parametrize("d", [320, 200])
+def test_f32_small_strip_many_token_and_vocab_chunks(d):
+    # float32 with a 256 x 256 residual strip: 700 tokens make three token chunks (the dW
+    # tiles of the second and third add into dW, and read H^T at a k-block offset of whole
+    # 32-wide blocks), every shard several vocabulary chunks, the residual stored at the
+    # Tc pitch.  d = 320 runs the direct-to-LDS logits tiles, d = 200 the register-staged
+    # ones.  Full dH and dW against the oracle at the float32 bar.
+    inp = _case("tiny_f32_T256_d256_V2048_P8", T=700, d=d, V=1900, P=1, seed=43)
+    inp = wl.resplit(inp, [611, 0, 300, 989], order=[2, 3, 0, 1])
+    g = wl.random_grad_loss(inp.T, 43, "random")
+    got = run_gpu(inp, g, strip_elems=256 * 256)
+    ref = run_oracle(inp, g)
+    errs = compare_all(inp, got, ref, f"f32 small strip d={d}")
+    print(f"f32 small strip d={d}:", errs, flush=True)
+
+
 def test_edge_targets_and_degenerate_cases():
     inp = _case("bf16_T4096_d2880_V201088_P8", T=130, d=64, V=600, P=1, seed=7)
     inp = wl.resplit(inp, [128, 128, 344], order=[2, 1, 0])
