@@ -108,6 +108,26 @@ vp_status vp_ce_forward(const vp_problem* prob, const void* H, const void* const
                         const int64_t* targets, float* loss, float* lse, void* ws,
                         size_t ws_bytes, void* stream);
 
+/* The forward for callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the same as
+ * vp_ce_forward, with the same kernels and results, but its workspace is a
+ * library-owned device buffer of 16 MiB per device (held from the first call on a
+ * device until the process ends), so the call allocates nothing.  The caller still
+ * passes H, the shards, the targets and the outputs.
+ *   - Returns VP_ERR_WORKSPACE before any work is enqueued if the problem's forward
+ *     workspace (vp_ce_workspace_size) exceeds 16 MiB (about T <= 460000 tokens at the
+ *     usual split counts).
+ *   - Every call on one device shares that device's buffer: calls that overlap on a
+ *     device (different streams or threads) race and give wrong results; calls
+ *     ordered on one stream are safe.
+ *   - The count of out-of-range targets is kept in that buffer and is not reported
+ *     (vp_ce_check needs a caller's workspace); such tokens still get a NaN loss.
+ *   - The first call on a device looks up the buffer's device address (no
+ *     allocation); VP_ERR_HIP if that fails. */
+vp_status vp_ce_forward_noalloc(const vp_problem* prob, const void* H,
+                                const void* const* W_shards, const int64_t* targets,
+                                float* loss, float* lse, void* stream);
+
 /* Backward (appendix on Ring-DTP: recompute each block of logits from the saved
  * normaliser, form the softmax residual, contract into both gradients):
  *   G[t, v]  = grad_loss[t] * (exp(y_tv - lse[t]) - [v == targets[t]]),

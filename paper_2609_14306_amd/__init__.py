@@ -25,7 +25,8 @@ VP_F32, VP_BF16 = 0, 1
 VP_ACCUMULATE_DW = 1
 VP_MAX_SHARDS = 64
 
-EXPORTED = ("vp_ce_workspace_size", "vp_ce_forward", "vp_ce_backward", "vp_ce_state_init",
+EXPORTED = ("vp_ce_workspace_size", "vp_ce_forward", "vp_ce_forward_noalloc", "vp_ce_backward",
+            "vp_ce_state_init",
             "vp_ce_fold_shard", "vp_ce_fold_finalize", "vp_ce_plan_info", "vp_ce_check",
             "vp_status_str", "vp_abi_version")
 
@@ -78,6 +79,8 @@ def load_library(path: str = LIB_PATH) -> ctypes.CDLL:
     lib.vp_ce_workspace_size.argtypes = [vp, P(ctypes.c_size_t), P(ctypes.c_size_t)]
     lib.vp_ce_forward.restype = ctypes.c_int
     lib.vp_ce_forward.argtypes = [vp, vptr, P(vptr), vptr, vptr, vptr, vptr, ctypes.c_size_t, vptr]
+    lib.vp_ce_forward_noalloc.restype = ctypes.c_int
+    lib.vp_ce_forward_noalloc.argtypes = [vp, vptr, P(vptr), vptr, vptr, vptr, vptr]
     lib.vp_ce_backward.restype = ctypes.c_int
     lib.vp_ce_backward.argtypes = [vp, vptr, P(vptr), vptr, vptr, vptr, vptr, P(vptr), vptr,
                                    ctypes.c_size_t, vptr]
@@ -261,6 +264,18 @@ def vp_ce_forward(prob: Problem, H, W_shards, targets, loss, lse, ws, stream=Non
                                       _ptr(loss), _ptr(lse), _ptr(ws), ws.numel() * ws.element_size(),
                                       _stream(stream))
     _check(st, "vp_ce_forward")
+
+
+def vp_ce_forward_noalloc(prob: Problem, H, W_shards, targets, loss, lse, stream=None) -> None:
+    """vp_ce_forward with the library's own 16 MiB device workspace (no allocation)."""
+    import torch
+    named = _check_inputs(prob, H, W_shards, targets)
+    _need(loss, "loss", torch.float32, (prob.T,))
+    _need(lse, "lse", torch.float32, (prob.T,))
+    _same_device(named + [("loss", loss), ("lse", lse)])
+    st = load_library().vp_ce_forward_noalloc(ctypes.byref(prob.c), _ptr(H), _ptr_array(W_shards),
+                                              _ptr(targets), _ptr(loss), _ptr(lse), _stream(stream))
+    _check(st, "vp_ce_forward_noalloc")
 
 
 def vp_ce_backward(prob: Problem, H, W_shards, targets, lse, grad_loss, dH, dW_shards, ws,

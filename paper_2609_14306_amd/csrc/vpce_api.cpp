@@ -223,22 +223,29 @@ vp_status vp_ce_workspace_size(const vp_problem* prob, size_t* fwd_bytes, size_t
   return VP_OK;
 }
 
-vp_status vp_ce_forward(const vp_problem* prob, const void* H, const void* const* W_shards,
-                        const int64_t* targets, float* loss, float* lse, void* ws,
-                        size_t ws_bytes, void* stream) {
-  int64_t V = 0;
-  vp_status st = validate(prob, &V);
+}  // extern "C"
+
+namespace {
+
+// Argument checks of the forward shared by vp_ce_forward and vp_ce_forward_noalloc
+// (everything except the workspace).
+vp_status check_forward(const vp_problem* prob, const void* H, const void* const* W_shards,
+                        const int64_t* targets, float* loss, float* lse, int64_t* V) {
+  vp_status st = validate(prob, V);
   if (st != VP_OK) return st;
   if ((st = check_shards(prob, W_shards)) != VP_OK) return st;
-  if (!ws) return VP_ERR_WORKSPACE;
-  if (ws_bytes < fwd_ws_bytes(prob)) return VP_ERR_WORKSPACE;
-  if (misaligned(ws)) return VP_ERR_ALIGN;
-  const int64_t T = prob->T;
-  if (T > 0) {
+  if (prob->T > 0) {
     if (!H || !targets || !loss || !lse) return VP_ERR_NULL;
     if (misaligned(H)) return VP_ERR_ALIGN;
   }
-  hipStream_t s = (hipStream_t)stream;
+  return VP_OK;
+}
+
+// The forward on a checked problem, with a workspace of at least fwd_ws_bytes(prob).
+vp_status forward_impl(const vp_problem* prob, int64_t V, const void* H,
+                       const void* const* W_shards, const int64_t* targets, float* loss,
+                       float* lse, void* ws, hipStream_t s) {
+  const int64_t T = prob->T;
   unsigned long long* counter = (unsigned long long*)ws;
   if (!vpce::run_ws_init(counter, s)) return VP_ERR_HIP;
   if (T == 0) return VP_OK;
@@ -274,6 +281,36 @@ vp_status vp_ce_forward(const vp_problem* prob, const void* H, const void* const
   c.bad_counter = counter;
   if (!vpce::run_comb(c, s)) return VP_ERR_HIP;
   return VP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+vp_status vp_ce_forward(const vp_problem* prob, const void* H, const void* const* W_shards,
+                        const int64_t* targets, float* loss, float* lse, void* ws,
+                        size_t ws_bytes, void* stream) {
+  int64_t V = 0;
+  vp_status st = validate(prob, &V);
+  if (st != VP_OK) return st;
+  if ((st = check_shards(prob, W_shards)) != VP_OK) return st;
+  if (!ws) return VP_ERR_WORKSPACE;
+  if (ws_bytes < fwd_ws_bytes(prob)) return VP_ERR_WORKSPACE;
+  if (misaligned(ws)) return VP_ERR_ALIGN;
+  if ((st = check_forward(prob, H, W_shards, targets, loss, lse, &V)) != VP_OK) return st;
+  return forward_impl(prob, V, H, W_shards, targets, loss, lse, ws, (hipStream_t)stream);
+}
+
+vp_status vp_ce_forward_noalloc(const vp_problem* prob, const void* H,
+                                const void* const* W_shards, const int64_t* targets,
+                                float* loss, float* lse, void* stream) {
+  int64_t V = 0;
+  const vp_status st = check_forward(prob, H, W_shards, targets, loss, lse, &V);
+  if (st != VP_OK) return st;
+  if (fwd_ws_bytes(prob) > vpce::kScratchBytes) return VP_ERR_WORKSPACE;
+  void* ws = nullptr;
+  if (!vpce::scratch_base(&ws)) return VP_ERR_HIP;
+  return forward_impl(prob, V, H, W_shards, targets, loss, lse, ws, (hipStream_t)stream);
 }
 
 vp_status vp_ce_state_init(float* state, int64_t T, void* stream) {

@@ -121,6 +121,12 @@ struct TileShape {
 };
 
 TileShape tile_shape(int dtype);
+
+// Bytes of the library-owned device workspace of vp_ce_forward_noalloc.
+constexpr size_t kScratchBytes = 16u << 20;
+// Device address of that workspace on the current device (looked up on the first
+// call per device and kept); false if the lookup fails.
+bool scratch_base(void** out);
 bool run_ws_init(unsigned long long* counter, hipStream_t s);
 bool run_fill_zero(float* p, int64_t n, hipStream_t s);
 bool run_fwd(int dtype, const FwdArgs& a, hipStream_t s);

@@ -22,6 +22,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include <mutex>
+
 #include "vpce_internal.h"
 
 namespace vpce {
@@ -1120,6 +1122,33 @@ static bool launch_stage(const GemmArgs& h, const GemmArgs& w, const GradArgs& g
   using Mm = typename Cfg<E>::Mm;
   if (g.d % Cfg<E>::Logits::KDIV == 0) return launch_stage_g<E, typename Cfg<E>::Logits, Mm>(h, w, g, s);
   return launch_stage_g<E, typename Cfg<E>::LogitsReg, Mm>(h, w, g, s);
+}
+
+// ---------------------------------------------------------------------------
+// Library-owned forward workspace for callers that cannot allocate (see
+// vp_ce_forward_noalloc).  Each device the library runs on holds its own copy
+// from the first use until the process ends.  In host code `scratch` names a
+// host-side stand-in, not device memory: its device address is looked up once
+// per device with hipGetSymbolAddress, and only that address is ever passed on.
+static __device__ __align__(256) unsigned char scratch[kScratchBytes];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_addr[kMaxDevices] = {};
+}  // namespace
+
+bool scratch_base(void** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return false;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (!scratch_addr[dev]) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)) != hipSuccess || !p) return false;
+    scratch_addr[dev] = p;
+  }
+  *out = scratch_addr[dev];
+  return true;
 }
 
 // ---- entry points used by the host API (vpce_api.cpp) ----

@@ -246,3 +246,23 @@ def test_fold_argument_errors_before_launch():
 def test_check_null_workspace():
     lib = vp.load_library()
     assert lib.vp_ce_check(None, None, None) == vp.VP_ERR_NULL
+
+
+def test_forward_noalloc_refusals_before_launch():
+    lib = vp.load_library()
+
+    def call(prob, H=FAKE, W=None, t=FAKE, loss=FAKE, lse=FAKE):
+        Wa = (ctypes.c_void_p * max(prob.P, 1))(*(W or [FAKE] * prob.P))
+        return lib.vp_ce_forward_noalloc(ctypes.byref(prob.c), H, Wa, t, loss, lse, 0)
+
+    # the problem's forward workspace exceeds the library's 16 MiB buffer
+    big = _prob(T=(1 << 23) - 256, shard_rows=[1000])
+    assert vp.vp_ce_workspace_size(big)[0] > 16 << 20
+    assert call(big) == vp.VP_ERR_WORKSPACE
+    p = _prob(shard_rows=[100])
+    assert call(p, H=None) == vp.VP_ERR_NULL
+    assert call(p, loss=None) == vp.VP_ERR_NULL
+    assert call(p, H=FAKE + 2) == vp.VP_ERR_ALIGN
+    assert call(p, W=[FAKE + 4]) == vp.VP_ERR_ALIGN
+    assert lib.vp_ce_forward_noalloc(None, FAKE, None, FAKE, FAKE, FAKE, 0) == vp.VP_ERR_NULL
+    assert call(_prob(shard_rows=[100], order=[1])) == vp.VP_ERR_ORDER
