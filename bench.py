@@ -314,6 +314,11 @@ def main():
     wall = time.perf_counter() - t0
     fwd_ms = [e[0].elapsed_time(e[1]) for e in evs]
     bwd_ms = [e[1].elapsed_time(e[2]) for e in evs]
+    step_ev_ms = [e[0].elapsed_time(e[2]) for e in evs]
+
+    def stats(xs):
+        return {"mean": float(np.mean(xs)), "median": float(np.median(xs)), "min": float(np.min(xs)),
+                "max": float(np.max(xs))}
     gpu_ms = evs[0][0].elapsed_time(evs[-1][2]) / args.steps
     ms_per_step = max(wall * 1e3 / args.steps, gpu_ms)
     flops = 8.0 * T * V * d
@@ -345,6 +350,8 @@ def main():
         "pct_peak": 100.0 * tflops / peak,
         "fwd_ms": fwd_avg,
         "bwd_ms": bwd_avg,
+        # per-step HIP-event times on the launch stream (forward call, backward call, both)
+        "timing_ms": {"fwd": stats(fwd_ms), "bwd": stats(bwd_ms), "fwd_bwd": stats(step_ev_ms)},
         "working_set_mib": {"workspace_fwd": fwd_b / 2**20, "workspace_bwd": bwd_b / 2**20,
                             "allocated_during_steps": extra_alloc / 2**20,
                             "peak_over_resident": (max(fwd_b, bwd_b) + extra_alloc) / 2**20},

@@ -32,4 +32,7 @@ def test_bench_line():
     cpu = d["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["value"] > 0 and cpu["cores"] >= 1
     assert d["working_set_mib"]["allocated_during_steps"] == 0
+    for part in ("fwd", "bwd", "fwd_bwd"):
+        t = d["timing_ms"][part]
+        assert 0 < t["min"] <= t["median"] <= t["max"] and t["min"] <= t["mean"] <= t["max"]
     assert d["bad_targets"] == 0
