@@ -99,7 +99,7 @@ size_t fwd_ws_bytes(const vp_problem* p) {
 // on V.
 struct StripPlan {
   int64_t Tc, Vc, T_pad;
-  size_t off_g[2], off_gt[2], off_ht, off_wt, total;
+  size_t off_g[2], off_gt[2], off_ht, off_wt, off_yt, total;
 };
 
 StripPlan strip_plan(const vp_problem* p) {
@@ -122,7 +122,8 @@ StripPlan strip_plan(const vp_problem* p) {
   }
   s.off_ht = off;
   s.off_wt = s.off_ht + align256((size_t)p->d * s.T_pad * eb);
-  s.total = s.off_wt + align256((size_t)p->d * s.Vc * eb);
+  s.off_yt = s.off_wt + align256((size_t)p->d * s.Vc * eb);
+  s.total = s.off_yt + align256((size_t)T * 4);
   return s;
 }
 
@@ -472,6 +473,21 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
     if (!vpce::run_transpose(prob->dtype, tr, s)) return VP_ERR_HIP;
   }
 
+  float* yt = (float*)(wsb + plan.off_yt);
+  {  // the target logit of every token, read by the residual tiles for the one-hot term
+    vpce::TgtArgs ta;
+    memset(&ta, 0, sizeof(ta));
+    int32_t n_tiles = 0;
+    build_table(prob, W_shards, ts.grad_bm, &ta.st, &n_tiles);
+    ta.H = H;
+    ta.targets = targets;
+    ta.T = T;
+    ta.V = V;
+    ta.d = (int32_t)d;
+    ta.yt = yt;
+    if (!vpce::run_target_logits(prob->dtype, ta, s)) return VP_ERR_HIP;
+  }
+
   const std::vector<Chunk> chunks = strip_chunks(prob, plan);
   int64_t off[VP_MAX_SHARDS];
   int64_t acc = 0;
@@ -505,6 +521,7 @@ vp_status vp_ce_backward(const vp_problem* prob, const void* H, const void* cons
       g.gid0 = off[c.q] + c.v0;
       g.V = V;
       g.ignore_index = prob->ignore_index;
+      g.yt = yt;
       g.M = (int32_t)c.M;
       g.N = (int32_t)c.N;
       g.d = (int32_t)d;

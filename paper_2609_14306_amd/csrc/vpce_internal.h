@@ -79,10 +79,22 @@ struct GradArgs {
   int64_t t0;      // first token of this chunk
   int64_t gid0;    // global id of the chunk's first row
   int64_t V, ignore_index;
+  const float* yt;  // [T] target logit h_t . w_{targets[t]} of every token (0 if none)
   int32_t M;       // vocabulary rows in this chunk
   int32_t N;       // tokens in this chunk
   int32_t d;
   int32_t n_vt;    // vocabulary tiles over M
+};
+
+// Target logits: yt[t] = h_t . w_{targets[t]} for targets in [0, V), 0 otherwise.  The
+// shard table may list the shards in any order.
+struct TgtArgs {
+  ShardTable st;
+  const void* H;
+  const int64_t* targets;
+  int64_t T, V;
+  int32_t d;
+  float* yt;
 };
 
 // C[M][N] = (beta ? C : 0) + A B^T with A [M][K] (row stride lda) and B [N][K]
@@ -146,5 +158,6 @@ struct StageSplit {
 bool run_bwd_stage(int dtype, const GemmArgs& h, const GemmArgs& w, const GradArgs& g,
                    hipStream_t s);
 bool run_transpose(int dtype, const TransposeArgs& a, hipStream_t s);
+bool run_target_logits(int dtype, const TgtArgs& a, hipStream_t s);
 
 }  // namespace vpce

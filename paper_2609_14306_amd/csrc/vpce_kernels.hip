@@ -23,6 +23,7 @@
 #include <stdint.h>
 
 #include <mutex>
+#include <type_traits>
 
 #include "vpce_internal.h"
 
@@ -422,12 +423,17 @@ struct GemmDma {
     wait_slices(pro - 1);
     __builtin_amdgcn_s_barrier();
     const char* ring = (const char*)smem;
-    F16 a[2][MB], b[2][NB];
+    // A fragments are single-buffered: each is re-read for the next sub-step right
+    // after its last MFMA of this one.  B fragments are double-buffered and read
+    // during the first MFMAs of the sub-step.  The MFMAs go in snake order (row
+    // block i takes its column blocks forwards for even i, backwards for odd i), so
+    // that consecutive MFMAs share an operand.
+    F16 a[MB], b[2][NB];
 #pragma unroll
     for (int idx = 0; idx < NR; ++idx) {
       const F16 f = read_one(ring, wm, wn, 0, lane, idx);
       if (idx < MB)
-        a[0][idx] = f;
+        a[idx] = f;
       else
         b[0][idx - MB] = f;
     }
@@ -461,21 +467,17 @@ struct GemmDma {
         const int dslice = kk == NKK - 1 ? kt + STAGES : kt + STAGES - 1;
         const bool dvalid = (kk == NKK - 1 || (kk == 0 && kt >= 1)) && dslice < nk;
         __builtin_amdgcn_sched_barrier(0);
-        // One MFMA, then one fragment read for the next sub-step, then (every other
-        // MFMA) one load: the wave never holds a burst of memory instructions in
-        // front of its next MFMA.
+        // One MFMA, then the fragment reads it frees for the next sub-step, then
+        // (every other MFMA) one load: the wave never holds a burst of memory
+        // instructions in front of its next MFMA.
 #pragma unroll
         for (int idx = 0; idx < NM; ++idx) {
-          const int i = idx / NB, j = idx % NB;
-          if (!RAGGED || i < mb_live) acc[i][j] = E::mma16(a[cur][i], b[cur][j], acc[i][j]);
+          const int i = idx / NB, jj = idx % NB, j = (i & 1) ? NB - 1 - jj : jj;
+          const bool live = !RAGGED || i < mb_live;
+          if (live) acc[i][j] = E::mma16(a[i], b[cur][j], acc[i][j]);
           __builtin_amdgcn_sched_barrier(0);
-          if (idx < NR && (!RAGGED || idx >= MB || idx < mb_live)) {
-            const F16 f = read_one(src, wm, wn, skk, lane, idx);
-            if (idx < MB)
-              a[cur ^ 1][idx] = f;
-            else
-              b[cur ^ 1][idx - MB] = f;
-          }
+          if (idx < NB) b[cur ^ 1][idx] = read_one(src, wm, wn, skk, lane, MB + idx);
+          if (jj == NB - 1 && live) a[i] = read_one(src, wm, wn, skk, lane, i);
           if ((idx & 1) == 0 && idx / 2 < HALF && (kk == NKK - 1 || kk == 0) && dvalid)
             issue_one(L, dslice, dq0 + idx / 2, lds0, wave);
           __builtin_amdgcn_sched_barrier(0);
@@ -580,8 +582,11 @@ __global__ void __launch_bounds__(G::NT, G::OCC) fwd_kernel(FwdArgs a) {
     G::run(acc, Wt, a.d, 0, rows, (const S*)a.H, a.d, n0, (int)a.T, a.d, smem);
 
     // Tiles past the end of a shard mask their padded rows; full tiles (all but the
-    // last of each shard) take the select-free loops.
+    // last of each shard) take the select-free loops.  Register r of row block i
+    // holds tile row wm + 32 i + acc_row(r, lane) = wm + 4 (lane / 32) + (a constant),
+    // so the mask compares that constant with one per-lane limit.
     const bool full = rows == BM;
+    const int lim = rows - wm - 4 * (lane >> 5);
 #pragma unroll
     for (int j = 0; j < NB; ++j) {
       // The maximum is taken on the raw logits and scaled once: scaling by a positive
@@ -598,7 +603,7 @@ __global__ void __launch_bounds__(G::NT, G::OCC) fwd_kernel(FwdArgs a) {
         for (int i = 0; i < MB; ++i)
 #pragma unroll
           for (int r = 0; r < 16; ++r)
-            if (wm + 32 * i + acc_row(r, lane) < rows) tmax = fmaxf(tmax, acc[i][j][r]);
+            if (32 * i + 8 * (r >> 2) + (r & 3) < lim) tmax = fmaxf(tmax, acc[i][j][r]);
       }
       tmax *= kLog2e;
       const float scale = tmax > m_run[j] ? __builtin_amdgcn_exp2f(m_run[j] - tmax) : 1.f;
@@ -616,7 +621,7 @@ __global__ void __launch_bounds__(G::NT, G::OCC) fwd_kernel(FwdArgs a) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r], kLog2e, -m_run[j]));
-            sum += (wm + 32 * i + acc_row(r, lane) < rows) ? e : 0.f;
+            sum += (32 * i + 8 * (r >> 2) + (r & 3) < lim) ? e : 0.f;
           }
       }
       s_run[j] = s_run[j] * scale + sum;
@@ -769,13 +774,21 @@ __device__ __forceinline__ void store_tile_blocked(const uint16_t* lds, uint16_t
 }
 
 // Backward residual: recompute a logits tile of the (vocabulary chunk, token
-// chunk) strip and store G = g (2^(y log2e - lse log2e) - onehot) into the strip
-// in both layouts: G[v][t] (token columns contiguous, for dW) and G^T[t][v]
-// (vocabulary columns contiguous, for dH).  Rows and columns of the tile that
-// fall outside the chunk are written as zeros so that both contractions can
-// read whole 16-byte chunks past a ragged edge.  bfloat16 tiles go through LDS
-// (free once the mainloop returns) once per layout, so that both layouts leave
-// as whole 16-byte chunks, 1 KiB per wavefront store.
+// chunk) strip and store G = g (softmax - onehot) into the strip in both layouts:
+// G[v][t] (token columns contiguous, for dW) and G^T[t][v] (vocabulary columns
+// contiguous, for dH).  Rows and columns of the tile that fall outside the chunk
+// are written as zeros so that both contractions can read whole 16-byte chunks
+// past a ragged edge.
+//
+// Every element is first written as g p = sign(g) 2^(y log2e + log2|g| - lse log2e)
+// (one multiply-add and one exponential: the upstream gradient is folded into the
+// exponent, and an ignored token gets log2|g| = -inf, i.e. zeros); the one element
+// of a token column that holds its target is then overwritten, by the one lane that
+// owns it, with g (p_t - 1) computed in float32 from the token's target logit yt
+// (a separate dot product; it agrees with the tile's own value up to float32
+// summation order).  bfloat16 tiles go through LDS (free once the mainloop returns)
+// once per layout, so that both layouts leave as whole 16-byte chunks, 1 KiB per
+// wavefront store; the target elements are patched in LDS before each store.
 template <class E, class G>
 __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
                                           typename E::storage* smem) {
@@ -803,28 +816,51 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
     static_assert(BM == 256 && BN == 256, "the LDS staging holds one 256 x 256 tile");
     static_assert(G::LDS_ELEMS >= BM * BN, "the ring must hold one bfloat16 tile");
   }
-  // G values of this lane, bfloat16 bits packed two per word: packed[j][i][r4/4]
-  // holds vocabulary rows ml0 .. ml0 + 3 of token column nl.
-  uint2 packed[NB][MB][4];
+  const bool full = m0 + BM <= a.M;  // no padding rows: no row mask
+  // row mask of the last tile of a chunk: register group r4 of row block i holds rows
+  // m0 + wm + 4 (lane / 32) + 32 i + 8 (r4 / 4) + q
+  const int lim = a.M - m0 - wm - 4 * (lane >> 5);
+  // Per token column j of this lane: the exponent offset, the sign of g, and the
+  // target element this lane owns (tile row, or -1) with its value.
+  float cexp[NB], vt_val[NB];
+  uint32_t sgn[NB];
+  int trow[NB];
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int nl = n0 + wn + 32 * j + (lane & 31);  // token column within the chunk
-    float lse2 = 0.f, g = 0.f;
-    int rel = -1;  // target row within the chunk, or -1
-    bool live = false, bad = false;
+    cexp[j] = -INFINITY;
+    sgn[j] = 0u;
+    trow[j] = -1;
+    vt_val[j] = 0.f;
     if (nl < a.N) {
       const int64_t t = a.t0 + nl;
       const int64_t tg = a.targets[t];
       if (tg != a.ignore_index) {
-        bad = tg < 0 || tg >= a.V;
-        live = true;
-        lse2 = a.lse[t] * kLog2e;
-        g = a.grad[t];
-        const int64_t r64 = tg - a.gid0;
-        rel = (r64 >= 0 && r64 < a.M) ? (int)r64 : -1;
+        float g = a.grad[t];
+        if (tg < 0 || tg >= a.V) g = __builtin_nanf("");  // out of range: NaN row
+        const float lse2 = a.lse[t] * kLog2e;
+        const float ag = __builtin_fabsf(g);
+        cexp[j] = __builtin_amdgcn_logf(ag) - lse2;  // log2|g| - lse log2e
+        sgn[j] = g < 0.f ? 0x80008000u : 0u;
+        // the target element: tile row rel - m0, in this wave's rows and this lane half
+        const int64_t rel = tg - a.gid0 - m0 - wm;
+        if (rel >= 0 && rel < G::WM && (int)((rel >> 2) & 1) == (lane >> 5)) {
+          trow[j] = (int)rel + wm;
+          const float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(a.yt[t], kLog2e, -lse2));
+          vt_val[j] = g * (pt - 1.f);
+        }
       }
     }
-    if (bad) g = __builtin_nanf("");
+  }
+  // G values of this lane, bfloat16 bits packed two per word: packed[j][i][r4/4]
+  // holds vocabulary rows ml0 .. ml0 + 3 of token column nl.  Full tiles take the
+  // loop without the padding-row mask.
+  uint2 packed[NB][MB][4];
+  auto residual = [&](auto masked) {
+    constexpr bool MASKED = decltype(masked)::value;
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int nl = n0 + wn + 32 * j + (lane & 31);
 #pragma unroll
     for (int i = 0; i < MB; ++i)
 #pragma unroll
@@ -834,25 +870,41 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
         float v4[4];
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          const int ml = ml0 + q;
-          const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r4 + q], kLog2e, -lse2));
-          v4[q] = (live && ml < a.M) ? g * (p - (rel == ml ? 1.f : 0.f)) : 0.f;
-          if constexpr (!kBlocked)
-            Gs[(((uint32_t)nl / KB) * Vc + (uint32_t)ml) * KB + (uint32_t)nl % KB] = v4[q];
+          const float e = __builtin_amdgcn_exp2f(__builtin_fmaf(acc[i][j][r4 + q], kLog2e, cexp[j]));
+          v4[q] = (!MASKED || 32 * i + r4 / 4 * 8 + q < lim) ? e : 0.f;
         }
         if constexpr (kBlocked) {
-          packed[j][i][r4 >> 2].x = E::pack2(v4[0], v4[1]);
-          packed[j][i][r4 >> 2].y = E::pack2(v4[2], v4[3]);
-        } else {  // 4 consecutive vocabulary rows: one 16-byte store into a 32-wide k-block
+          packed[j][i][r4 >> 2].x = E::pack2(v4[0], v4[1]) ^ sgn[j];
+          packed[j][i][r4 >> 2].y = E::pack2(v4[2], v4[3]) ^ sgn[j];
+        } else {
+          const float sg = sgn[j] ? -1.f : 1.f;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            v4[q] *= sg;
+            Gs[(((uint32_t)nl / KB) * Vc + (uint32_t)(ml0 + q)) * KB + (uint32_t)nl % KB] = v4[q];
+          }
+          // 4 consecutive vocabulary rows: one 16-byte store into a 32-wide k-block
           *(float4*)(Gt + (((uint32_t)ml0 / KB) * Tc + (uint32_t)nl) * KB + (uint32_t)ml0 % KB) =
               make_float4(v4[0], v4[1], v4[2], v4[3]);
         }
       }
+    if constexpr (!kBlocked) {
+      if (trow[j] >= 0) {  // the target element, after this lane's own stores of it
+        const uint32_t ml = (uint32_t)(m0 + trow[j]);
+        Gs[(((uint32_t)nl / KB) * Vc + ml) * KB + (uint32_t)nl % KB] = vt_val[j];
+        Gt[((ml / KB) * Tc + (uint32_t)nl) * KB + ml % KB] = vt_val[j];
+      }
+    }
   }
+  };
+  if (full)
+    residual(std::false_type{});
+  else
+    residual(std::true_type{});
   if constexpr (kBlocked) {
     uint16_t* lds = (uint16_t*)smem;
     // G^T: the tile as rows of tokens, columns of vocabulary ids; a lane's 4
-    // consecutive ids are one 8-byte write.
+    // consecutive ids are one 8-byte write; then the target elements.
 #pragma unroll
     for (int j = 0; j < NB; ++j)
 #pragma unroll
@@ -862,6 +914,13 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
           const int tl = wn + 32 * j + (lane & 31), vl = wm + 32 * i + acc_row(r4, lane);
           *(uint2*)((char*)lds + tile_lds_byte(tl, vl)) = packed[j][i][r4 >> 2];
         }
+    uint16_t tbits[NB];
+#pragma unroll
+    for (int j = 0; j < NB; ++j) {
+      tbits[j] = (uint16_t)(E::pack2(vt_val[j], 0.f) & 0xFFFFu);
+      if (trow[j] >= 0)
+        *(uint16_t*)((char*)lds + tile_lds_byte(wn + 32 * j + (lane & 31), trow[j])) = tbits[j];
+    }
     __syncthreads();
     store_tile_blocked<G::NT>(lds, Gt, (uint32_t)m0 >> 6, Tc, (uint32_t)n0);
     __syncthreads();
@@ -880,9 +939,51 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
           *(uint16_t*)(base + tile_lds_byte(vl + 2, tl)) = (uint16_t)(p.y & 0xFFFFu);
           *(uint16_t*)(base + tile_lds_byte(vl + 3, tl)) = (uint16_t)(p.y >> 16);
         }
+#pragma unroll
+    for (int j = 0; j < NB; ++j)
+      if (trow[j] >= 0)
+        *(uint16_t*)((char*)lds + tile_lds_byte(trow[j], wn + 32 * j + (lane & 31))) = tbits[j];
     __syncthreads();
     store_tile_blocked<G::NT>(lds, Gs, (uint32_t)n0 >> 6, Vc, (uint32_t)m0);
   }
+}
+
+// yt[t] = h_t . w_{targets[t]} (float32 sum of the exact products), one wavefront per
+// token, 16-byte loads (d is a multiple of 8).  Targets outside [0, V) (ignored or out
+// of range) give 0; the residual tiles do not use it for them.
+template <class S>
+__global__ void __launch_bounds__(256) target_logit_kernel(TgtArgs a) {
+  constexpr int VEC = 16 / (int)sizeof(S);
+  const int64_t t = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (t >= a.T) return;
+  const int64_t tg = a.targets[t];
+  float acc = 0.f;
+  if (tg >= 0 && tg < a.V) {
+    int p = 0;
+    while (p + 1 < a.st.P && !(tg >= a.st.off[p] && tg < a.st.off[p] + a.st.rows[p])) ++p;
+    const S* w = (const S*)a.st.w[p] + (tg - a.st.off[p]) * (int64_t)a.d;
+    const S* h = (const S*)a.H + t * (int64_t)a.d;
+    for (int k = lane * VEC; k < a.d; k += 64 * VEC) {
+      const uint4 hv = *(const uint4*)(h + k), wv = *(const uint4*)(w + k);
+      if constexpr (sizeof(S) == 2) {
+        const uint32_t hh[4] = {hv.x, hv.y, hv.z, hv.w}, ww[4] = {wv.x, wv.y, wv.z, wv.w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc = __builtin_fmaf(__uint_as_float(hh[q] << 16), __uint_as_float(ww[q] << 16), acc);
+          acc = __builtin_fmaf(__uint_as_float(hh[q] & 0xFFFF0000u), __uint_as_float(ww[q] & 0xFFFF0000u), acc);
+        }
+      } else {
+        acc = __builtin_fmaf(__uint_as_float(hv.x), __uint_as_float(wv.x), acc);
+        acc = __builtin_fmaf(__uint_as_float(hv.y), __uint_as_float(wv.y), acc);
+        acc = __builtin_fmaf(__uint_as_float(hv.z), __uint_as_float(wv.z), acc);
+        acc = __builtin_fmaf(__uint_as_float(hv.w), __uint_as_float(wv.w), acc);
+      }
+    }
+  }
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) acc += __shfl_xor(acc, o);
+  if (lane == 0) a.yt[t] = acc;
 }
 
 // Counts out-of-range targets of a token range (backward's copy of the check).
@@ -1219,6 +1320,15 @@ bool run_count_bad(const int64_t* targets, int64_t T, int64_t V, int64_t ignore_
 bool run_bwd_stage(int dtype, const GemmArgs& h, const GemmArgs& w, const GradArgs& g,
                    hipStream_t s) {
   return dtype == 1 ? launch_stage<Bf16>(h, w, g, s) : launch_stage<F32>(h, w, g, s);
+}
+bool run_target_logits(int dtype, const TgtArgs& a, hipStream_t s) {
+  if (a.T <= 0) return true;
+  const dim3 grid((unsigned)((a.T + 3) / 4));
+  if (dtype == 1)
+    hipLaunchKernelGGL(target_logit_kernel<uint16_t>, grid, dim3(256), 0, s, a);
+  else
+    hipLaunchKernelGGL(target_logit_kernel<float>, grid, dim3(256), 0, s, a);
+  return launched_ok();
 }
 bool run_transpose(int dtype, const TransposeArgs& a, hipStream_t s) {
   if (a.C <= 0 || a.R_pad <= 0) return true;
