@@ -842,9 +842,10 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
         const float ag = __builtin_fabsf(g);
         cexp[j] = __builtin_amdgcn_logf(ag) - lse2;  // log2|g| - lse log2e
         sgn[j] = g < 0.f ? 0x80008000u : 0u;
-        // the target element: tile row rel - m0, in this wave's rows and this lane half
+        // the target element: inside the chunk (its padding rows stay zero), in this
+        // wave's rows of the tile and in this lane half
         const int64_t rel = tg - a.gid0 - m0 - wm;
-        if (rel >= 0 && rel < G::WM && (int)((rel >> 2) & 1) == (lane >> 5)) {
+        if (tg - a.gid0 < a.M && rel >= 0 && rel < G::WM && (int)((rel >> 2) & 1) == (lane >> 5)) {
           trow[j] = (int)rel + wm;
           const float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(a.yt[t], kLog2e, -lse2));
           vt_val[j] = g * (pt - 1.f);
