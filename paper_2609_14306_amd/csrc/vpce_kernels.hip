@@ -299,9 +299,10 @@ struct GemmDma {
   static constexpr int B_LOADS = BN / RPI / NWAVES;
   static_assert(BM % (RPI * NWAVES) == 0 && BN % (RPI * NWAVES) == 0, "whole load groups per wave");
   static constexpr int NLOADS = A_LOADS + B_LOADS;  // per wave and slice
-  static_assert(NLOADS % 2 == 0, "loads go out in two halves");
+  // the loads of a slice go out in two halves, the larger first
+  static constexpr int HALF0 = (NLOADS + 1) / 2, HALF1 = NLOADS - HALF0;
   static constexpr int NM = MB * NB, NR = MB + NB;   // MFMAs and fragment reads per sub-step
-  static_assert(NR <= NM && NLOADS / 2 <= (NM + 1) / 2, "interleave slots");
+  static_assert(NR <= NM && HALF0 <= (NM + 1) / 2, "interleave slots");
   static constexpr int LDS_ELEMS = STAGES * SLICE_BYTES / (int)sizeof(S);
   static_assert(STAGES * SLICE_BYTES <= 160 * 1024, "LDS");
 
@@ -462,8 +463,8 @@ struct GemmDma {
         // last sub-step of slice kt (after the barrier: every wave has finished
         // reading slice kt, whose slot they refill), the second during the first
         // sub-step of slice kt+1 (the prologue issued the first STAGES slices).
-        constexpr int HALF = NLOADS / 2;
-        const int dq0 = kk == NKK - 1 ? 0 : HALF;
+        const int dq0 = kk == NKK - 1 ? 0 : HALF0;
+        const int dn = kk == NKK - 1 ? HALF0 : HALF1;
         const int dslice = kk == NKK - 1 ? kt + STAGES : kt + STAGES - 1;
         const bool dvalid = (kk == NKK - 1 || (kk == 0 && kt >= 1)) && dslice < nk;
         __builtin_amdgcn_sched_barrier(0);
@@ -478,7 +479,7 @@ struct GemmDma {
           __builtin_amdgcn_sched_barrier(0);
           if (idx < NB) b[cur ^ 1][idx] = read_one(src, wm, wn, skk, lane, MB + idx);
           if (jj == NB - 1 && live) a[i] = read_one(src, wm, wn, skk, lane, i);
-          if ((idx & 1) == 0 && idx / 2 < HALF && (kk == NKK - 1 || kk == 0) && dvalid)
+          if ((idx & 1) == 0 && idx / 2 < dn && (kk == NKK - 1 || kk == 0) && dvalid)
             issue_one(L, dslice, dq0 + idx / 2, lds0, wave);
           __builtin_amdgcn_sched_barrier(0);
         }
@@ -999,8 +1000,27 @@ __global__ void count_bad_kernel(const int64_t* targets, int64_t T, int64_t V, i
 
 // One float32 output tile of C = (beta ? C : 0) + A B^T (a dH or a dW tile; N, the
 // hidden width, is a multiple of 4).
+// Column blocks of a dH / dW contraction, whose N is the hidden width d: BM-wide
+// tiles of C^T rows (GM), except that a remainder of at most GW::BM - GM::BM
+// columns joins the last full block, which then runs as one GW::BM-wide tile
+// instead of leaving a block that is mostly padding (d = 2880: ten 256-wide
+// blocks and one 320-wide block, not twelve 256-wide blocks of which the last
+// holds 64 live columns).
+struct ColBlocks {
+  int n;      // column blocks
+  bool wide;  // the last block is a GW tile
+};
+template <class GM, class GW>
+__host__ __device__ inline ColBlocks col_blocks(int N) {
+  static_assert(GW::BM > GM::BM && GW::BN == GM::BN, "the wide tile only widens C^T rows");
+  const int full = N / GM::BM, rem = N % GM::BM;
+  if (full >= 1 && rem > 0 && rem <= GW::BM - GM::BM) return ColBlocks{full, true};
+  return ColBlocks{(N + GM::BM - 1) / GM::BM, false};
+}
+
+// One tile of C (+)= A B^T: rows m0 = mt * BN .. of C, columns n0 .. n0 + BM - 1.
 template <class E, class G, bool RAGGED = false>
-__device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int nt,
+__device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int n0,
                                           typename E::storage* smem) {
   using S = typename E::storage;
   constexpr int MB = G::MB, NB = G::NB;
@@ -1009,7 +1029,7 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int nt,
   // The tile is computed transposed, C^T[n][m] = sum_k B[n][k] A[m][k]: accumulator
   // rows run along n, so each lane's group of 4 registers holds 4 consecutive
   // columns of one row of C and the epilogue moves 16 bytes per access.
-  const int n0 = nt * G::BM, m0 = mt * G::BN;
+  const int m0 = mt * G::BN;
   f32x16_t acc[MB][NB];
 #pragma unroll
   for (int i = 0; i < MB; ++i)
@@ -1048,28 +1068,37 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int nt,
 // tiles (numbered from first[.][x]): every XCD gets an even share of each kind,
 // consecutive tiles of one kind stay on one XCD's L2, and the longest tiles go
 // first so that the partly filled last round is made of the short ones.
-template <class E, class GL, class GM>
+template <class E, class GL, class GM, class GW>
 __global__ void __launch_bounds__(GM::NT, GM::OCC)
     bwd_stage_kernel(GemmArgs h, GemmArgs w, GradArgs g, StageSplit sp) {
-  static_assert(GL::NT == GM::NT, "one workgroup size for every tile kind");
+  static_assert(GL::NT == GM::NT && GW::NT == GM::NT, "one workgroup size for every tile kind");
   using S = typename E::storage;
-  constexpr int LDS = GL::LDS_ELEMS > GM::LDS_ELEMS ? GL::LDS_ELEMS : GM::LDS_ELEMS;
+  constexpr int LDS0 = GL::LDS_ELEMS > GM::LDS_ELEMS ? GL::LDS_ELEMS : GM::LDS_ELEMS;
+  constexpr int LDS = LDS0 > GW::LDS_ELEMS ? LDS0 : GW::LDS_ELEMS;
   __shared__ __attribute__((aligned(16))) S smem[LDS];
   const int xcd = blockIdx.x % 8;
   int local = blockIdx.x / 8;
   int mt, nt;
-  // dH (kind 0) and dW (kind 1) tiles; a tile of the last column block that reaches
-  // past the hidden width d runs ragged: the waves' row blocks past d do no MFMA work.
+  // dH (kind 0) and dW (kind 1) tiles (see col_blocks); a tile that reaches past the
+  // hidden width d runs ragged: the waves' row blocks past d do no MFMA work.
 #pragma unroll
   for (int k = 0; k < 2; ++k) {
     const GemmArgs& a = k == 0 ? h : w;
     if (local < sp.cnt[k][xcd]) {
-      const int n_n = (a.N + GM::BM - 1) / GM::BM, n_m = (a.M + GM::BN - 1) / GM::BN;
-      grouped_tile(sp.first[k][xcd] + local, n_m, n_n, 4, mt, nt);
-      if ((nt + 1) * GM::BM > a.N)
-        gemm_tile<E, GM, true>(a, mt, nt, smem);
-      else
-        gemm_tile<E, GM>(a, mt, nt, smem);
+      const ColBlocks cb = col_blocks<GM, GW>(a.N);
+      const int n_m = (a.M + GM::BN - 1) / GM::BN;
+      grouped_tile(sp.first[k][xcd] + local, n_m, cb.n, 4, mt, nt);
+      const int n0 = nt * GM::BM;
+      if (cb.wide && nt == cb.n - 1) {
+        if (n0 + GW::BM > a.N)
+          gemm_tile<E, GW, true>(a, mt, n0, smem);
+        else
+          gemm_tile<E, GW>(a, mt, n0, smem);
+      } else if (n0 + GM::BM > a.N) {
+        gemm_tile<E, GM, true>(a, mt, n0, smem);
+      } else {
+        gemm_tile<E, GM>(a, mt, n0, smem);
+      }
       return;
     }
     local -= sp.cnt[k][xcd];
@@ -1142,6 +1171,9 @@ template <> struct Cfg<Bf16> {
   // pipe.
   using Logits = GemmDma<256, 256, 2, 4>;
   using Mm = Logits;  // the dH / dW contractions
+  // the last dH / dW column block when d leaves 1..64 columns past a multiple of
+  // 256 (160 x 64 per wave, 0.7 fragment reads per MFMA)
+  using MmWide = GemmDma<320, 256, 2, 4>;
   using LogitsReg = Gemm<Bf16, Logits::BM, Logits::BN, Logits::WGM, Logits::WGN>;
   static_assert(64 % Mm::KDIV == 0, "dH / dW launch granularity");
   static constexpr int KALIGN = 64;  // K granularity the dH / dW launches need
@@ -1152,6 +1184,7 @@ template <> struct Cfg<F32> {
   // register-staged tile of the same shape.
   using Logits = GemmDma<256, 256, 2, 4, 64, 2, F32>;
   using Mm = Logits;  // the dH / dW contractions
+  using MmWide = GemmDma<320, 256, 2, 4, 64, 2, F32>;
   using LogitsReg = Gemm<F32, Logits::BM, Logits::BN, Logits::WGM, Logits::WGN>;
   static constexpr int KALIGN = 32;  // K granularity the dH / dW launches need
 };
@@ -1203,27 +1236,29 @@ static StageSplit split_stage(const int n_kind[3]) {
   return sp;
 }
 
-template <class E, class GL, class GM>
+template <class E, class GL, class GM, class GW>
 static bool launch_stage_g(const GemmArgs& h, const GemmArgs& w, const GradArgs& g, hipStream_t s) {
-  auto tiles = [](const GemmArgs& a, int bm, int bn) {
-    return a.M > 0 ? ((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn) : 0;
+  auto tiles = [](const GemmArgs& a) {  // C^T tiles: column blocks along N, BN along M
+    return a.M > 0 ? ((a.M + GM::BN - 1) / GM::BN) * col_blocks<GM, GW>(a.N).n : 0;
   };
   int n_kind[3];
-  n_kind[0] = tiles(h, GM::BN, GM::BM);  // C^T tiles: BM along N, BN along M
-  n_kind[1] = tiles(w, GM::BN, GM::BM);
+  n_kind[0] = tiles(h);
+  n_kind[1] = tiles(w);
   n_kind[2] = g.M > 0 ? g.n_vt * ((g.N + GL::BN - 1) / GL::BN) : 0;
   const int n = n_kind[0] + n_kind[1] + n_kind[2];
   if (n == 0) return true;
   const StageSplit sp = split_stage(n_kind);
-  hipLaunchKernelGGL((bwd_stage_kernel<E, GL, GM>), dim3((unsigned)n), dim3(GM::NT), 0, s, h, w,
-                     g, sp);
+  hipLaunchKernelGGL((bwd_stage_kernel<E, GL, GM, GW>), dim3((unsigned)n), dim3(GM::NT), 0, s, h,
+                     w, g, sp);
   return launched_ok();
 }
 template <class E>
 static bool launch_stage(const GemmArgs& h, const GemmArgs& w, const GradArgs& g, hipStream_t s) {
   using Mm = typename Cfg<E>::Mm;
-  if (g.d % Cfg<E>::Logits::KDIV == 0) return launch_stage_g<E, typename Cfg<E>::Logits, Mm>(h, w, g, s);
-  return launch_stage_g<E, typename Cfg<E>::LogitsReg, Mm>(h, w, g, s);
+  using Wd = typename Cfg<E>::MmWide;
+  if (g.d % Cfg<E>::Logits::KDIV == 0)
+    return launch_stage_g<E, typename Cfg<E>::Logits, Mm, Wd>(h, w, g, s);
+  return launch_stage_g<E, typename Cfg<E>::LogitsReg, Mm, Wd>(h, w, g, s);
 }
 
 // ---------------------------------------------------------------------------

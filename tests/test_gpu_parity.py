@@ -25,12 +25,13 @@ def test_tiny_f32_full_workload():
     assert got["bad_fwd"] == 0 and got["bad_bwd"] == 0
 
 
-@pytest.mark.parametrize("d", [200, 448, 576])
+@pytest.mark.parametrize("d", [200, 320, 448, 544, 576])
 @pytest.mark.parametrize("dtype_name", ["tiny_f32_T256_d256_V2048_P8", "bf16_T4096_d2880_V201088_P8"])
 def test_ragged_shards_and_tiles(dtype_name, d):
     # T, d and every shard length off the tile grid; an empty shard; a permuted order.
-    # The last 256-wide column block of the dH / dW tiles holds 200, 192 and 64 live
-    # rows of d, so its tiles issue 4, 3 and 1 of the 4 A load groups of a slice.
+    # The dH / dW column blocks of d: 200 and 448 end in a 256-wide block with 200 and
+    # 192 live rows; 320 and 576 end in a whole 320-wide block (the first is the only
+    # block); 544 ends in a 320-wide block with 288 live rows.
     inp = _case(dtype_name, T=333, d=d, V=1100, P=1, seed=3)
     inp = wl.resplit(inp, [100, 0, 257, 131, 612], order=[3, 0, 4, 1, 2])
     g = wl.random_grad_loss(inp.T, 3, "random")
