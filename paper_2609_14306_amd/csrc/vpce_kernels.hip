@@ -1037,28 +1037,47 @@ __device__ __forceinline__ void gemm_tile(const GemmArgs& a, int mt, int n0,
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
   G::template run<RAGGED>(acc, (const S*)a.B, a.ldb, n0, a.N, (const S*)a.A, a.lda, m0, a.M, a.K, smem,
                           a.kblkb, a.kblka);
+  // The epilogue takes a lane's row of C a batch of IB row blocks at a time: all
+  // old values of the batch (beta = 1) are loaded before the first sum is stored,
+  // so the lane waits for memory once per batch rather than once per 16-byte chunk
+  // (a store to C ahead of the next load of C would keep the two in order).  Only
+  // a RAGGED tile has columns at or past N.
+  constexpr int IB = MB <= 4 ? MB : (MB + 1) / 2;
+  const bool beta = a.beta != 0;
 #pragma unroll
   for (int j = 0; j < NB; ++j) {
     const int m = m0 + wn + 32 * j + (lane & 31);
     if (m >= a.M) continue;
     float* crow = a.C + (int64_t)m * a.ldc;
 #pragma unroll
-    for (int i = 0; i < MB; ++i)
+    for (int i0 = 0; i0 < MB; i0 += IB) {
+      float4 old[IB][4];
 #pragma unroll
-      for (int r4 = 0; r4 < 16; r4 += 4) {
-        const int n = n0 + wm + 32 * i + acc_row(r4, lane);  // n .. n+3; N % 4 == 0
-        if (n >= a.N) continue;
-        float4 v = make_float4(acc[i][j][r4], acc[i][j][r4 + 1], acc[i][j][r4 + 2], acc[i][j][r4 + 3]);
-        float4* p = (float4*)(crow + n);
-        if (a.beta) {
-          const float4 c = *p;
-          v.x += c.x;
-          v.y += c.y;
-          v.z += c.z;
-          v.w += c.w;
-        }
-        *p = v;
+      for (int ii = 0; ii < IB; ++ii)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) old[ii][q] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if (beta) {
+#pragma unroll
+        for (int ii = 0; ii < IB; ++ii)
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            const int i = i0 + ii;
+            const int n = n0 + wm + 32 * i + acc_row(4 * q, lane);  // n .. n+3; N % 4 == 0
+            if (i < MB && (!RAGGED || n < a.N)) old[ii][q] = *(const float4*)(crow + n);
+          }
       }
+#pragma unroll
+      for (int ii = 0; ii < IB; ++ii)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          const int i = i0 + ii;
+          const int n = n0 + wm + 32 * i + acc_row(4 * q, lane);
+          if (i >= MB || (RAGGED && n >= a.N)) continue;
+          const float4 c = old[ii][q];
+          *(float4*)(crow + n) = make_float4(acc[i][j][4 * q] + c.x, acc[i][j][4 * q + 1] + c.y,
+                                             acc[i][j][4 * q + 2] + c.z, acc[i][j][4 * q + 3] + c.w);
+        }
+    }
   }
 }
 
