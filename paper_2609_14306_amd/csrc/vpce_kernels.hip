@@ -799,12 +799,31 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
   const int wm = G::wave_m(wave), wn = G::wave_n(wave);
   const int m0 = vt * BM, n0 = tb * BN;
 
+  // The per-token inputs of this lane's token columns are loaded ahead of the
+  // mainloop, which drains them with its own loads, so that their latency is not
+  // paid after it.  Columns past the chunk read its last token (N >= 1 whenever a
+  // residual tile runs) and are masked below.
+  int64_t tgv[NB];
+  float gv[NB], lsev[NB], ytv[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    const int64_t t = a.t0 + min(n0 + wn + 32 * j + (lane & 31), a.N - 1);
+    tgv[j] = a.targets[t];
+    gv[j] = a.grad[t];
+    lsev[j] = a.lse[t];
+    ytv[j] = a.yt[t];
+  }
+
   f32x16_t acc[MB][NB];
 #pragma unroll
   for (int i = 0; i < MB; ++i)
 #pragma unroll
     for (int j = 0; j < NB; ++j) acc[i][j] = f32x16_t{};
   G::run(acc, (const S*)a.W, a.d, m0, a.M, (const S*)a.H + a.t0 * a.d, a.d, n0, a.N, a.d, smem);
+  // (keeps the compiler from moving arithmetic on the prefetched values, and the wait
+  // it needs, in front of the mainloop)
+#pragma unroll
+  for (int j = 0; j < NB; ++j) asm volatile("" : "+v"(tgv[j]), "+v"(gv[j]), "+v"(lsev[j]), "+v"(ytv[j]));
 
   // Strip offsets fit in 32 bits (the strip budget is capped below 2^31 elements).
   // Both strips are k-blocked (see GradArgs) with KB = E::KB elements per block.
@@ -834,12 +853,11 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
     trow[j] = -1;
     vt_val[j] = 0.f;
     if (nl < a.N) {
-      const int64_t t = a.t0 + nl;
-      const int64_t tg = a.targets[t];
+      const int64_t tg = tgv[j];
       if (tg != a.ignore_index) {
-        float g = a.grad[t];
+        float g = gv[j];
         if (tg < 0 || tg >= a.V) g = __builtin_nanf("");  // out of range: NaN row
-        const float lse2 = a.lse[t] * kLog2e;
+        const float lse2 = lsev[j] * kLog2e;
         const float ag = __builtin_fabsf(g);
         cexp[j] = __builtin_amdgcn_logf(ag) - lse2;  // log2|g| - lse log2e
         sgn[j] = g < 0.f ? 0x80008000u : 0u;
@@ -848,7 +866,7 @@ __device__ __forceinline__ void grad_tile(const GradArgs& a, int vt, int tb,
         const int64_t rel = tg - a.gid0 - m0 - wm;
         if (tg - a.gid0 < a.M && rel >= 0 && rel < G::WM && (int)((rel >> 2) & 1) == (lane >> 5)) {
           trow[j] = (int)rel + wm;
-          const float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(a.yt[t], kLog2e, -lse2));
+          const float pt = __builtin_amdgcn_exp2f(__builtin_fmaf(ytv[j], kLog2e, -lse2));
           vt_val[j] = g * (pt - 1.f);
         }
       }
