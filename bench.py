@@ -48,7 +48,62 @@ def parse():
                     help="instead of the bench line, compare the fused path with the dense standard "
                          "(full logits, float32 log-softmax cross-entropy, autograd) on the same "
                          "workload: time and peak memory above the resident tensors")
+    ap.add_argument("--gemm-reference", action="store_true",
+                    help="instead of the bench line, time the fused forward against the library "
+                         "GEMM (torch.matmul, i.e. hipBLASLt) of the same logits, alternately, "
+                         "on the same operands")
     return ap.parse_args()
+
+
+def gemm_reference(inp, H, Ws, tg, steps: int, warmup: int):
+    """The fused forward against a plain library GEMM of the same operands.  The reference
+    computes every shard's logits W_q H^T with torch.matmul (hipBLASLt), written out in the
+    input dtype and not folded; the fused forward computes the same products and folds them
+    into the online log-sum-exp instead of writing them.  The two alternate, `steps` times
+    each after `warmup` rounds, in one process on the same resident operands, and both are
+    counted at 2 T V d flops.  The reference is plain torch beside the product, not part of
+    it."""
+    import numpy as np
+    import torch
+
+    import paper_2609_14306_amd as vp
+
+    torch.backends.cuda.matmul.allow_tf32 = False  # float32 products stay float32
+    T, d, V = inp.T, inp.d, inp.V
+    Ht = H.t()
+    C = torch.empty(max(w.shape[0] for w in Ws), T, dtype=H.dtype, device=H.device)
+    prob = vp.problem_for(H, Ws, inp.ignore_index, inp.order)
+    ws = torch.empty(vp.vp_ce_workspace_size(prob)[0], dtype=torch.uint8, device=H.device)
+    loss = torch.empty(T, dtype=torch.float32, device=H.device)
+    lse = torch.empty_like(loss)
+
+    def gemm():
+        for w in Ws:
+            torch.matmul(w, Ht, out=C[: w.shape[0]])
+
+    def fused():
+        vp.vp_ce_forward(prob, H, Ws, tg, loss, lse, ws)
+
+    times = {"gemm": [], "fused_forward": []}
+    for k in range(warmup + steps):
+        for name, fn in (("gemm", gemm), ("fused_forward", fused)):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            if k >= warmup:
+                times[name].append(e0.elapsed_time(e1))
+    flops = 2.0 * T * V * d
+    out = {}
+    for name, xs in times.items():
+        out[name] = {"median_ms": float(np.median(xs)), "min_ms": float(np.min(xs)),
+                     "tflops_at_median": flops / (float(np.median(xs)) * 1e-3) / 1e12}
+    out["fused_over_gemm_rate"] = out["gemm"]["median_ms"] / out["fused_forward"]["median_ms"]
+    out["gemm_what"] = (f"torch.matmul(W_q, H.t()) for each of the {len(Ws)} shards, "
+                        f"{inp.dtype} output")
+    return out
 
 
 def standard_vs_fused(inp, H, Ws, tg, steps: int, warmup: int, keep_outputs: bool = False):
@@ -268,10 +323,14 @@ def main():
     Ws = [to_dev(x) for x in inp.W_shards]
     tg = torch.from_numpy(inp.targets).to(dev)
     T, d, V = inp.T, inp.d, inp.V
-    if args.standard:
-        res = standard_vs_fused(inp, H, Ws, tg, args.steps, args.warmup)
-        res.update({"mode": "standard_vs_fused", "workload": w.name, "T": T, "d": d, "V": V,
-                    "steps": args.steps, "warmup": args.warmup})
+    if args.standard or args.gemm_reference:
+        if args.standard:
+            res = standard_vs_fused(inp, H, Ws, tg, args.steps, args.warmup)
+        else:
+            res = gemm_reference(inp, H, Ws, tg, args.steps, args.warmup)
+        res.update({"mode": "standard_vs_fused" if args.standard else "gemm_reference",
+                    "workload": w.name, "T": T, "d": d, "V": V, "steps": args.steps,
+                    "warmup": args.warmup})
         print(json.dumps(res), flush=True)
         return
     n_valid = int((inp.targets != inp.ignore_index).sum())

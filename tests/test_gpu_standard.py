@@ -14,6 +14,9 @@ that rounding: |d loss| <= 2^-8 (1 + max_v |y_tv|) per token (the log-sum-exp an
 the target logit each move by at most the largest logit rounding, 2^-9 |y|);
 its gradients, like the fused leg's, go through a bfloat16 residual (<= 1e-2).
 The dense float32 leg meets the float32 bar.
+
+The --gemm-reference mode (the fused forward alternating with torch.matmul of the same
+logits) is checked for the fields it reports.
 """
 import json
 import os
@@ -80,3 +83,18 @@ def test_standard_mode_json_line():
         assert d[leg]["ms_per_step"] > 0 and d[leg]["peak_above_resident_mib"] > 0
     assert d["dense_logits_fp32_mib"] == 256 * 2048 * 4 / 2**20
     assert "outputs" not in d
+
+
+def test_gemm_reference_mode_json_line():
+    # bench.py --gemm-reference: the fused forward alternating with torch.matmul of the same
+    # logits; both timed, both counted at 2 T V d.
+    r = subprocess.run([sys.executable, os.path.join(ROOT, "bench.py"), "--gemm-reference",
+                        "--workload", "tiny_f32_T256_d256_V2048_P8", "--steps", "2", "--warmup", "1"],
+                       capture_output=True, text=True, timeout=300, cwd=ROOT)
+    assert r.returncode == 0, r.stderr[-2000:]
+    d = json.loads([ln for ln in r.stdout.splitlines() if ln.startswith("{")][-1])
+    assert d["mode"] == "gemm_reference" and d["workload"] == "tiny_f32_T256_d256_V2048_P8"
+    for leg in ("gemm", "fused_forward"):
+        assert 0 < d[leg]["min_ms"] <= d[leg]["median_ms"]
+        assert d[leg]["tflops_at_median"] > 0
+    assert d["fused_over_gemm_rate"] > 0
