@@ -1200,12 +1200,11 @@ __global__ void __launch_bounds__(256) transpose_kernel(TransposeArgs a) {
 template <class E> struct Cfg;
 template <> struct Cfg<Bf16> {
   // 512-thread workgroups (two wavefronts per SIMD), 256 x 256 tiles, 128 x 64 per
-  // wave, for every contraction (d = 2880 pads the dH / dW column tiles to 3072:
-  // measured faster inside the backward stage launch than 256 x 192 tiles with
-  // 64 x 96 per wave, whose fragment reads per MFMA are higher).  One wavefront
-  // per SIMD with 128 x 128 per wave reads a third less LDS per MFMA but measured
-  // 17% slower: a lone wave's load-issue stalls and barrier waits idle the MFMA
-  // pipe.
+  // wave, for every contraction (measured faster inside the backward stage launch
+  // than 256 x 192 tiles with 64 x 96 per wave, whose fragment reads per MFMA are
+  // higher).  One wavefront per SIMD with 128 x 128 per wave reads a third less LDS
+  // per MFMA and runs at a higher clock, but measured 5-17% slower: a lone wave's
+  // load waits and barrier waits idle the MFMA pipe.
   using Logits = GemmDma<256, 256, 2, 4>;
   using Mm = Logits;  // the dH / dW contractions
   // the last dH / dW column block when d leaves 1..64 columns past a multiple of
