@@ -278,10 +278,21 @@ def cpu_baseline(inp, rows: int):
     t0 = time.perf_counter()
     oracle.forward_backward(H, Ws, inp.targets[:rows], g, inp.ignore_index)
     dt = time.perf_counter() - t0
+    cpu_model = None
+    try:
+        with open("/proc/cpuinfo") as f:
+            for ln in f:
+                if ln.startswith("model name"):
+                    cpu_model = ln.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     return {"value": rows / dt, "unit": "tokens/s", "cores": int(cores), "kind": "oracle",
             "sample": f"first {rows} of {inp.T} tokens at full V={inp.V}, d={inp.d} "
                       f"(float64 forward+backward, {dt:.2f} s)",
-            "seconds": dt}
+            "seconds": dt, "nproc": os.cpu_count(), "cpu_model": cpu_model,
+            # the oracle's three products (logits, dH, dW): 6 rows V d float64 operations
+            "gflops": 6.0 * rows * inp.V * inp.d / dt / 1e9}
 
 
 def main():

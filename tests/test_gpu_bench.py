@@ -31,6 +31,7 @@ def test_bench_line():
     assert roof["traffic"] is None  # the committed counter profile covers another workload
     cpu = d["cpu_baseline"]
     assert cpu["kind"] == "oracle" and cpu["value"] > 0 and cpu["cores"] >= 1
+    assert cpu["gflops"] > 0 and cpu["nproc"] >= 1 and "cpu_model" in cpu
     assert d["working_set_mib"]["allocated_during_steps"] == 0
     for part in ("fwd", "bwd", "fwd_bwd"):
         t = d["timing_ms"][part]
