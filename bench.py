@@ -257,6 +257,14 @@ def measured_clock(kernel: str, workload: str):
             "source": os.path.relpath(MFMA_PROFILE, ROOT)}
 
 
+def add_frac_at_clock(roof: dict, dtype: str) -> None:
+    """The achieved rate against the MFMA peak at the clock the counters saw (bf16 only: the
+    counter profile covers the bf16 long-context workload)."""
+    c = roof.get("counters")
+    if c is not None and dtype == "bf16":
+        c["frac_at_clock"] = roof["achieved"] / c["peak_at_clock"]
+
+
 def cpu_baseline(inp, rows: int):
     """The oracle as it stands, on the first `rows` tokens (full V and d): its cost is linear in T."""
     import numpy as np
@@ -458,6 +466,7 @@ def main():
         r = out[key]
         r["traffic_gb_per_s"] = (r["traffic"] / (r["avg_launch_ms"] * 1e-3) / 1e9
                                  if r["traffic"] is not None else None)
+        add_frac_at_clock(r, inp.dtype)
     if not args.no_cpu_baseline:
         out["cpu_baseline"] = cpu_baseline(inp, args.cpu_sample_rows)
     print(json.dumps(out), flush=True)

@@ -52,6 +52,19 @@ def test_clock_and_occupancy(tmp_path, monkeypatch):
     assert bench.measured_clock("fwd_kernel", WL) is None
 
 
+def test_frac_at_clock(tmp_path, monkeypatch):
+    p = tmp_path / "mfma.md"
+    _summary(p, bench.kernel_source_sha256(),
+             extra=[("fwd_kernel_clock_ghz", "1.5"), ("fwd_kernel_mfma_busy", "0.75")])
+    monkeypatch.setattr(bench, "MFMA_PROFILE", str(p))
+    roof = {"achieved": 1000.0, "counters": bench.measured_clock("fwd_kernel", WL)}
+    bench.add_frac_at_clock(roof, "bf16")
+    assert abs(roof["counters"]["frac_at_clock"] - 1000.0 / (bench.PEAK_BF16_TFLOPS * 1.5 / 2.4)) < 1e-12
+    roof = {"achieved": 1000.0, "counters": None}
+    bench.add_frac_at_clock(roof, "bf16")  # no profile for this kernel source: nothing added
+    assert roof["counters"] is None
+
+
 def test_committed_profiles_name_the_default_workload():
     # the committed summaries cover the workload bench.py runs by default
     for path in (bench.TRAFFIC_PROFILE, bench.MFMA_PROFILE):
